@@ -1,0 +1,142 @@
+/*
+ * als.h -- one ALS half-sweep on an AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the update-X step of alternating least squares for the weighted-lambda
+ * cost function (eq. 1) of Tan, Cao and Fong, "Faster and Cheaper: Parallelizing Large-Scale
+ * Matrix Factorization on GPUs" (HPDC'16): for every row u of the sparse m x n rating matrix R,
+ *
+ *     A_u = sum over stored (u,v) of (theta_v theta_v^T + lambda I)  =  G_u + lambda n_u I
+ *     b_u = Theta^T R_u*^T  =  sum over stored (u,v) of r_uv theta_v
+ *     x_u = A_u^{-1} b_u                                         (eq. 2, Algorithm 1)
+ *
+ * The update-Theta step (eq. 3) is the same call on the transposed matrix (CSC of R) with the
+ * roles of X and Theta exchanged.
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers on the context's device, owned by the caller.
+ *     The library never allocates or frees device memory; its only scratch is the workspace
+ *     handed to als_init.
+ *   - Sparse matrices are CSR: rowptr int64[m+1] (rowptr[0] = 0, non-decreasing, rowptr[m] =
+ *     nnz), colidx int32[nnz] (0 <= colidx < n, no repeated column within a row), vals
+ *     fp32[nnz].  Every stored entry counts as a rating, whatever its value.
+ *   - Factor matrices are dense row-major fp32: Theta is n x f (theta_v contiguous, i.e. the
+ *     bytes of the paper's f x n Theta^T stored column-major), X is m x f.
+ *   - Pointers must be naturally aligned (8 bytes for int64, 4 bytes for int32/fp32), else
+ *     ALS_ERR_ALIGN.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Argument checks happen before the
+ *     call returns; all device work is queued on `stream` without a host synchronisation, so
+ *     inputs must stay valid until the stream has passed the call.
+ *   - Index ranges are not validated on the device; out-of-range colidx is undefined.
+ *   - No C++ exception crosses this interface.  Status codes are below; after ALS_ERR_HIP the
+ *     HIP error code is available from als_last_hip_error.
+ *   - A context serves one device and must not be used from two host threads at once; calls
+ *     queued on different streams of one context must not overlap in time (they share the
+ *     workspace).
+ */
+#ifndef ALS_H
+#define ALS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    ALS_OK = 0,
+    ALS_ERR_INVALID_ARG = -1,   /* null pointer, negative size, lambda < 0 or not finite   */
+    ALS_ERR_UNSUPPORTED_F = -2, /* f outside [1, ALS_F_MAX]                                 */
+    ALS_ERR_WORKSPACE = -3,     /* workspace missing or smaller than als_workspace_bytes    */
+    ALS_ERR_ALIGN = -4,         /* a pointer is not naturally aligned                        */
+    ALS_ERR_HIP = -5,           /* a HIP runtime call failed (see als_last_hip_error)        */
+    ALS_ERR_ALIAS = -6,         /* theta_in and x_out overlap                                */
+    ALS_ERR_DEVICE = -7         /* device index invalid or not a gfx950 device               */
+};
+
+#define ALS_F_MAX 128
+
+typedef struct als_ctx als_ctx;
+
+/* Bytes of device workspace a context on `device` needs for every f <= f_max.  Returns 0 if
+   the device cannot be queried or f_max is outside [1, ALS_F_MAX].  The size depends on the
+   device's compute-unit count and f_max only (not on m, n or nnz). */
+size_t als_workspace_bytes(int device, int32_t f_max);
+
+/* Create a context on `device` using the caller's device workspace (at least
+   als_workspace_bytes(device, f_max) bytes, 256-byte aligned; owned by the caller, who keeps
+   it alive until als_destroy).  f_max bounds the f of later calls. */
+int als_init(als_ctx** ctx, int device, void* workspace, size_t workspace_bytes, int32_t f_max);
+
+/* Release the context (not the workspace).  Does not synchronise. */
+int als_destroy(als_ctx* ctx);
+
+/*
+ * One half-sweep (eq. 2; Algorithm 1, Get_Hermitian_X then Batch_Solve):
+ *   x_out[u] = (sum_v theta_v theta_v^T + lambda n_u I)^{-1} sum_v r_uv theta_v
+ * for every row u in [0, m), v over the stored columns of row u, theta_v = theta_in[v].
+ *   rowptr, colidx, vals : CSR of the m x n matrix (see conventions)
+ *   theta_in             : n x f, read only; must not overlap x_out
+ *   x_out                : m x f, every row is written
+ *   lambda               : >= 0 and finite
+ * Rows with no stored entry get x_u = 0 (the paper does not define them; J does not depend
+ * on such an x_u).  A row whose A_u is not numerically positive definite (possible only when
+ * lambda = 0 or through overflow) gets NaN in x_u and is counted in the device counter that
+ * als_status reports.  The result does not depend on the stream, on earlier calls or on timing:
+ * the summation order is fixed.
+ */
+int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
+                   const float* vals, int64_t m, int64_t n, int32_t f, float lambda,
+                   const float* theta_in, float* x_out, void* stream);
+
+/*
+ * Training root-mean-square error over the stored entries (the evaluation metric of the
+ * paper's experiments, on the training set):
+ *   *rmse_out = sqrt( sum over stored (u,v) of (r_uv - x_u . theta_v)^2 / nnz )
+ * Residuals in fp32, sums in fp64 in a fixed order.  rmse_out is a DEVICE double; 0 when
+ * nnz = 0.
+ */
+int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
+             int64_t m, int64_t n, int32_t f, const float* x, const float* theta,
+             double* rmse_out, void* stream);
+
+/* Synchronise `stream`, then return (and reset to 0) the number of rows found not positive
+   definite by half-sweeps since the previous call. */
+int als_status(als_ctx* ctx, void* stream, int64_t* nonspd_rows);
+
+/*
+ * The row-to-wave partition a half-sweep with this f would use (integer work, exposed so it
+ * can be checked bit for bit).  Each row u costs c_row + c_nnz n_u units on a cost axis with
+ * prefix P(u) = c_nnz rowptr[u] + c_row u, T = P(m).  Boundary b of W waves sits at
+ * s_b = floor(T b / W): in row u_b, the largest u with P(u) <= s_b, at entry offset
+ * k_b = ceil((s_b - P(u_b) - c_row) / c_nnz) clamped to [0, n_u], rounded to the nearest
+ * multiple of q and, if not 0, moved to n_u when fewer than q/2 entries would remain.
+ * Wave w takes the entries from (u_w, k_w) up to (u_{w+1}, k_{w+1}); a row cut by a
+ * boundary is finished by a second pass that sums the pieces in wave order.
+ *   bounds_out : DEVICE int64[2 (W+1)], (u_b, k_b) pairs; capacity in pairs
+ *   params_out : HOST int64[4] = {W, c_nnz, c_row, q}
+ */
+int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t* bounds_out,
+             int64_t capacity, int64_t* params_out, void* stream);
+
+/*
+ * Measurement support (not part of the method).  After als_profile_begin, each of the next
+ * `capacity` half-sweeps records HIP events on its own stream around its three kernels (plan,
+ * herm_solve, reduce_solve).  als_profile_end synchronises on the last event, writes
+ * ms_out[3 i + 0..2] (HOST, capacity x 3 floats) for half-sweep i in call order, sets
+ * *count_out, and stops recording.
+ */
+int als_profile_begin(als_ctx* ctx, int32_t capacity);
+int als_profile_end(als_ctx* ctx, float* ms_out, int32_t capacity, int32_t* count_out);
+
+/* HIP error code of the most recent ALS_ERR_HIP on this context (0 if none). */
+int als_last_hip_error(const als_ctx* ctx);
+
+/* Static description of a status code. */
+const char* als_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALS_H */

@@ -1,0 +1,236 @@
+"""HIP half-sweep against the fp64 oracle, through the C ABI, on seeded synthetic inputs.
+
+Bar (per factor row): max_i |x_gpu - x_oracle| / max(max_i |x_oracle|, 1e-6 max |x_oracle|)
+<= 1e-3, the oracle fed the same fp32 inputs promoted to fp64.  Integer work (the partition)
+is compared bit for bit.  Item-side inputs are synthetic factors from the generator, never
+the GPU's own output.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import gpu_half_sweep, log, row_rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_1603_03820_amd import als
+    assert torch.cuda.is_available()
+    return als.Context(0, 128)
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.get()
+
+
+def synthetic_factor(rows, f, seed, std):
+    return synth.normal(seed, 8, (rows, f), std)
+
+
+def check_lockstep(ctx, orc, rowptr, colidx, vals, m, n, f, lam, theta, label, rows=None):
+    log(f"{label}: half-sweep m={m} n={n} nnz={int(rowptr[-1])} f={f} lam={lam}")
+    xg = gpu_half_sweep(ctx, rowptr, colidx, vals, m, n, f, lam, theta)
+    xo, st = orc.half_sweep(rowptr, colidx, vals, m, n, f, lam,
+                            np.asarray(theta, np.float64), rows=rows)
+    if rows is not None:
+        xg = xg[rows]
+    assert not np.isnan(xg).any(), f"{label}: unwritten or NaN rows"
+    err = row_rel_err(xg, xo)
+    worst = int(np.argmax(err))
+    assert err.max() <= TOL, f"{label}: row {worst} rel err {err.max():.3e}"
+    return xg, err
+
+
+def test_tiny_config_lockstep(ctx, orc):
+    p = synth.config("tiny")
+    check_lockstep(ctx, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, p.f, p.lam, p.theta0,
+                   "tiny user side")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, p.f, p.recipe["seed"], 0.3)
+    check_lockstep(ctx, orc, colptr, rowidx, vt, p.n, p.m, p.f, p.lam, xin, "tiny item side")
+
+
+RANKS = [1, 2, 3, 7, 16, 17, 31, 32, 33, 64, 100, 127, 128]
+
+
+@pytest.mark.parametrize("f", RANKS)
+def test_rank_lockstep_movie_shaped(ctx, orc, f):
+    # a scaled-down movie-shaped matrix: long item rows get cut across waves
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=777)
+    check_lockstep(ctx, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"movie-small f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 778, 1.0 / np.sqrt(f))
+    check_lockstep(ctx, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"movie-small f={f} item")
+
+
+def _handmade(lengths, n, seed):
+    rng = np.random.default_rng(seed)
+    rowptr = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    cols = [np.sort(rng.choice(n, size=k, replace=False)) for k in lengths]
+    colidx = np.concatenate(cols).astype(np.int32) if cols else np.zeros(0, np.int32)
+    vals = rng.uniform(1, 5, size=int(rowptr[-1])).astype(np.float32)
+    return rowptr, colidx, vals
+
+
+@pytest.mark.parametrize("f", [5, 16, 100, 128])
+def test_edge_row_lengths(ctx, orc, f):
+    n = 30_000
+    lengths = [0, 1, 2, f - 1, f, f + 1, 3, 63, 64, 65, 0, 127, 128, 129, 255, 256, 257, 0, 0,
+               511, 1000, 4095, 4096, 4097, 20_000, 1, 0]
+    lengths = [max(0, k) for k in lengths]
+    rowptr, colidx, vals = _handmade(lengths, n, seed=f)
+    theta = synthetic_factor(n, f, 91 + f, 0.2)
+    xg, _ = check_lockstep(ctx, orc, rowptr, colidx, vals, len(lengths), n, f, 0.05, theta,
+                           f"edge lengths f={f}")
+    empty = np.array(lengths) == 0
+    assert np.all(xg[empty] == 0.0)
+
+
+def test_partition_bit_exact(ctx, orc):
+    from paper_1603_03820_amd import als
+    cases = []
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=100, model="movie",
+                   plant_f=16, seed=777)
+    cases.append((p.rowptr, 100))
+    cases.append((p.csc()[0], 100))
+    cases.append((p.csc()[0], 16))
+    cases.append((np.zeros(9, np.int64), 64))
+    cases.append((np.array([0, 5, 5, 10_000, 10_001], np.int64), 128))
+    for rowptr, f in cases:
+        m = len(rowptr) - 1
+        log(f"plan m={m} nnz={int(rowptr[-1])} f={f}")
+        bounds, (W, c_nnz, c_row, q) = als.als_plan(ctx, to_dev(rowptr, ctx.device), m, f)
+        torch.cuda.synchronize()
+        ref = orc.partition(rowptr, m, W, c_nnz, c_row, q)
+        assert np.array_equal(bounds.cpu().numpy(), ref)
+
+
+def test_deterministic(ctx):
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=100, model="movie",
+                   plant_f=16, seed=777)
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, 100, 5, 0.1)
+    a = gpu_half_sweep(ctx, colptr, rowidx, vt, p.n, p.m, 100, 0.05, xin)
+    b = gpu_half_sweep(ctx, colptr, rowidx, vt, p.n, p.m, 100, 0.05, xin)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_not_spd_rows_are_nan_and_counted(ctx):
+    from paper_1603_03820_amd import als
+    # lambda = 0; columns 0..99 have theta_v[3:] = 0 exactly, so a row rating only those has an
+    # exactly singular Gram matrix (a zero pivot); columns 100..199 are generic.
+    f, n = 8, 200
+    theta = synthetic_factor(n, f, 17, 0.5)
+    theta[:100, 3:] = 0.0
+    rng = np.random.default_rng(4)
+    rows = [np.sort(rng.choice(100, 3, replace=False)),
+            np.sort(100 + rng.choice(100, 40, replace=False)),
+            np.zeros(0, np.int64),
+            np.array([7])]
+    rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int64)
+    colidx = np.concatenate(rows).astype(np.int32)
+    vals = rng.uniform(1, 5, len(colidx)).astype(np.float32)
+    als.als_status(ctx)   # clear
+    x = gpu_half_sweep(ctx, rowptr, colidx, vals, 4, n, f, 0.0, theta, sentinel=7.0)
+    assert np.all(np.isnan(x[0])) and np.all(np.isnan(x[3]))
+    assert np.all(np.isfinite(x[1])) and np.all(x[2] == 0.0)
+    assert als.als_status(ctx) == 2
+    assert als.als_status(ctx) == 0
+
+
+def test_empty_inputs(ctx):
+    from paper_1603_03820_amd import als
+    dev = ctx.device
+    # every row empty
+    rowptr = np.zeros(6, np.int64)
+    # (one-element index/value arrays: rowptr says there are no entries, none is read)
+    x = gpu_half_sweep(ctx, rowptr, np.zeros(1, np.int32), np.zeros(1, np.float32), 5, 3, 4,
+                       0.1, np.ones((3, 4), np.float32), sentinel=3.0)
+    assert np.all(x == 0.0)
+    # m = 0 is a no-op
+    z = torch.zeros(1, dtype=torch.int64, device=dev)
+    e = torch.zeros(1, dtype=torch.int32, device=dev)
+    v = torch.zeros(1, dtype=torch.float32, device=dev)
+    th = torch.ones(12, dtype=torch.float32, device=dev)
+    xo = torch.zeros(4, dtype=torch.float32, device=dev)
+    als.als_half_sweep(ctx, z, e, v, 0, 3, 4, 0.1, th, xo)
+    out = als.als_rmse(ctx, torch.zeros(6, dtype=torch.int64, device=dev), e, v, 5, 3, 4,
+                       torch.zeros(20, dtype=torch.float32, device=dev), th)
+    assert out.item() == 0.0
+
+
+def test_argument_errors(ctx):
+    from paper_1603_03820_amd import als
+    dev = ctx.device
+    rp = torch.tensor([0, 1], dtype=torch.int64, device=dev)
+    ci = torch.tensor([0], dtype=torch.int32, device=dev)
+    v = torch.tensor([1.0], dtype=torch.float32, device=dev)
+    th = torch.ones(256, dtype=torch.float32, device=dev)
+    x = torch.zeros(256, dtype=torch.float32, device=dev)
+
+    def code(fn):
+        with pytest.raises(als.ALSError) as ei:
+            fn()
+        return ei.value.code
+
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, 1, 1, 0, 0.1, th, x)) == -2
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, 1, 1, 129, 0.1, th, x)) == -2
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, 1, 1, 4, -1.0, th, x)) == -1
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, 1, 1, 4, float("nan"), th, x)) == -1
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, 1, 1, 4, 0.1, th, th[2:])) == -6
+    assert code(lambda: als.als_half_sweep(ctx, rp, ci, v, -1, 1, 4, 0.1, th, x)) == -1
+    # a float pointer one byte off its natural alignment
+    bad = torch.zeros(64, dtype=torch.uint8, device=dev)
+    import ctypes
+    rc = als._lib.als_half_sweep(ctx.handle, ctypes.c_void_p(rp.data_ptr()),
+                                 ctypes.c_void_p(ci.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+                                 1, 1, 4, ctypes.c_float(0.1), ctypes.c_void_p(th.data_ptr()),
+                                 ctypes.c_void_p(bad.data_ptr() + 1), None)
+    assert rc == -4
+
+
+def test_rmse_matches_oracle(ctx, orc):
+    from paper_1603_03820_amd import als
+    for f in (7, 100, 128):
+        p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                       plant_f=16, seed=31)
+        x = synthetic_factor(p.m, f, 32, 0.3)
+        th = synthetic_factor(p.n, f, 33, 0.3)
+        log(f"rmse f={f}")
+        dev = ctx.device
+        out = als.als_rmse(ctx, to_dev(p.rowptr, dev), to_dev(p.colidx, dev),
+                           to_dev(p.vals, dev), p.m, p.n, f, to_dev(x, dev), to_dev(th, dev))
+        ref = orc.rmse(p.rowptr, p.colidx, p.vals, p.m, f, x.astype(np.float64),
+                       th.astype(np.float64))
+        assert abs(out.item() - ref) <= 1e-6 * ref
+
+
+def test_tiny_trajectory_ten_iterations(ctx, orc):
+    """Free-running: ten iterations on each side from the same theta0; training RMSE agrees
+    within 1e-4 after every iteration."""
+    from paper_1603_03820_amd import driver
+    p = synth.config("tiny")
+    colptr, rowidx, vt = p.csc()
+    dp = driver.DeviceProblem.from_host(p.m, p.n, p.f, p.lam, p.rowptr, p.colidx, p.vals,
+                                        colptr, rowidx, vt, ctx.device)
+    log("tiny trajectory, 10 iterations")
+    x, th, hist = driver.train(ctx, dp, to_dev(p.theta0, ctx.device), p.iters)
+    theta = p.theta0.astype(np.float64)
+    ref = []
+    for _ in range(p.iters):
+        xo, theta = oracle.iterate(p.rowptr, p.colidx, p.vals, p.m, p.n, p.f, p.lam, theta,
+                                   csc=(colptr, rowidx, vt))
+        ref.append(orc.rmse(p.rowptr, p.colidx, p.vals, p.m, p.f, xo, theta))
+    diff = np.abs(np.array(hist) - np.array(ref))
+    assert diff.max() <= 1e-4, (hist, ref)
+    assert ref[-1] < ref[0]

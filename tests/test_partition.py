@@ -89,3 +89,62 @@ def test_partition_is_pure_integer_and_deterministic(oracle_lib):
     a = oracle_lib.partition(rowptr, 399, 97, 16, 1760, 256)
     b = oracle_lib.partition(rowptr, 399, 97, 16, 1760, 256)
     assert a.dtype == np.int64 and np.array_equal(a, b)
+
+
+def reducer_pieces(bounds, rowptr):
+    """The second pass's view: for each boundary that first cuts a row, the (wave, slot) pieces
+    it sums, as the reduce kernel selects them (slot 0 = a wave's first piece, 1 = its last)."""
+    m, W = len(rowptr) - 1, len(bounds) - 1
+
+    def cuts(b):
+        u, k = bounds[b]
+        return u < m and 0 < k < rowptr[u + 1] - rowptr[u]
+
+    out = {}
+    for b in range(1, W):
+        if not cuts(b):
+            continue
+        u = int(bounds[b][0])
+        if b > 1 and cuts(b - 1) and bounds[b - 1][0] == u:
+            continue
+        nu = int(rowptr[u + 1] - rowptr[u])
+        pieces = [(b - 1, 0 if bounds[b - 1][0] == u else 1)]
+        bb = b
+        while True:
+            more = bb + 1 < W and cuts(bb + 1) and bounds[bb + 1][0] == u
+            end = int(bounds[bb + 1][1]) if more else nu
+            if bounds[bb][1] < end:
+                pieces.append((bb, 0))
+            if not more:
+                break
+            bb += 1
+        out[u] = pieces
+    return out
+
+
+def writer_pieces(bounds, rowptr):
+    """What the first pass stores: (wave, slot) -> row, for every piece that is not a whole row."""
+    m = len(rowptr) - 1
+    stored = {}
+    for w, u, ka, kb in portions(bounds, rowptr):
+        nu = int(rowptr[u + 1] - rowptr[u])
+        if ka == 0 and kb == nu:
+            continue
+        slot = 0 if u == bounds[w][0] else 1
+        assert (w, slot) not in stored
+        stored[(w, slot)] = u
+    return stored
+
+
+@pytest.mark.parametrize("W", [3, 17, 200, 2000])
+def test_reducer_reads_exactly_the_stored_pieces(oracle_lib, W):
+    # few entries per wave: many boundaries snap onto the same cut point
+    rp = np.concatenate([[0], np.cumsum([3, 0, 5000, 1, 0, 300, 12000, 7, 900, 0, 4100])])
+    rp = rp.astype(np.int64)
+    bounds = oracle_lib.partition(rp, len(rp) - 1, W, 16, 16 * 60, 256)
+    stored = writer_pieces(bounds, rp)
+    read = reducer_pieces(bounds, rp)
+    read_set = {(w, s): u for u, ps in read.items() for (w, s) in ps}
+    assert read_set == stored
+    for u, ps in read.items():
+        assert [w for w, _ in ps] == sorted(w for w, _ in ps), "pieces summed in wave order"
