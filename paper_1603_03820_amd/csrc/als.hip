@@ -9,18 +9,21 @@
 //                   of a cost axis (see als_plan in als.h); no host synchronisation needed.
 //   k_herm_solve    per wave: walk its share row by row; gather theta_v for four entries at a
 //                   time straight into MFMA operand registers (lane = 16*k + column, so each
-//                   group of 16 lanes reads 64 contiguous bytes of one theta_v), accumulate the
-//                   lower block-triangle of the Gram matrix with v_mfma_f32_16x16x4_f32 and b_u
-//                   with VALU FMAs; rows that end in the share are regularised, factored
-//                   (Cholesky, folded forward substitution) and back-substituted in registers,
-//                   with a 16*NB-float LDS column buffer as the only broadcast medium.
+//                   group of 16 lanes reads 64 contiguous bytes of one theta_v), with the rating
+//                   appended as column f, and accumulate the upper block-triangle of the
+//                   augmented Gram matrix [A b; b^T c] with v_mfma_f32_16x16x4_f32.  Rows that
+//                   end in the share are regularised and solved in registers by a blocked
+//                   Cholesky: per 16-column block, the 16 x 16 diagonal tile is factored and
+//                   inverted with lane broadcasts, and the panel and trailing updates are
+//                   again 16x16x4 MFMAs; the forward substitution rides along as the augmented
+//                   column; the back substitution is a short blocked pass.
 //   k_reduce_solve  rows cut by share boundaries: sum the per-wave partial accumulators in
 //                   wave order (fixed, so results are reproducible), then the same solve.
 //   k_rmse_*        residuals per stored entry, fp64 partial sums in a fixed order.
 //
-// Register layout of the accumulators (the 16x16 MFMA C/D layout): tile (I,J), J <= I, lane l,
-// element r holds A[16 I + 4 (l >> 4) + r][16 J + (l & 15)].  The b accumulator of lane l holds
-// partial sums of b[16 J + (l & 15)] over the entries its 16-lane group saw.
+// Register layout of the accumulators (the 16x16 MFMA C/D layout): tile (I,J), I <= J, lane l,
+// element r holds M[16 I + 4 (l >> 4) + r][16 J + (l & 15)] of the augmented matrix M, whose
+// column f is b (and M[f][f] = sum r^2, unused).  NB = f/16 + 1 column blocks cover f + 1.
 
 #include <hip/hip_runtime.h>
 
@@ -37,23 +40,19 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kMaxNB = (ALS_F_MAX + 15) / 16;   // 8 column blocks of 16
+constexpr int kMaxNB = ALS_F_MAX / 16 + 1;      // 9 column blocks of 16 cover f + 1 <= 129
 constexpr int kSnap = 256;                      // partition cut grid (entries)
 constexpr int kCostPerEntry = 16;               // c_nnz
 constexpr int kMaxWavesPerCU = 32;
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
-constexpr int tix(int I, int J) { return I * (I + 1) / 2 + J; }   // J <= I
-// floats per partial-accumulator slot: tiles (4 per lane) + b (1 per block per lane)
-constexpr int slot_floats(int nb) { return (ntiles(nb) * 4 + nb) * kWave; }
-constexpr int lds_floats(int nb) { return 2 * (16 * nb + 4); }
+// upper block-triangle, row-major: tile (I, J) with I <= J
+constexpr int tu(int nb, int I, int J) { return I * nb - I * (I - 1) / 2 + (J - I); }
+// floats per partial-accumulator slot: tiles, 4 per lane
+constexpr int slot_floats(int nb) { return ntiles(nb) * 4 * kWave; }
 
 __device__ __forceinline__ float readlane_f(float v, int lane) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
-}
-
-__device__ __forceinline__ float pick4(const f4 v, int r) {
-    return r == 0 ? v[0] : (r == 1 ? v[1] : (r == 2 ? v[2] : v[3]));
 }
 
 // ------------------------------------------------------------------------------- plan ----
@@ -87,204 +86,294 @@ __global__ void k_plan(const int64_t* __restrict__ rowptr, int64_t m, int W, int
 
 // --------------------------------------------------------------------- Gram + RHS --------
 
-// theta values of one 4-entry step, as MFMA operands: lane (g, c) holds theta_{v_g}[16 I + c]
+// theta values of one 4-entry step, as MFMA operands: lane (g, c) loads theta_{v_g}[16 I + c].
+// The loads are unconditional (columns past f are clamped to a valid address, lanes past the
+// row's end read row 0); masking happens when the values are consumed, so the loads stay in
+// flight across the matrix ops of earlier steps.
 template <int NB>
-__device__ __forceinline__ void load_step(const float* __restrict__ theta, int f, int col,
-                                          bool ok, int c, float (&v)[NB]) {
+__device__ __forceinline__ void issue_step(const float* __restrict__ theta, int f, int col,
+                                           const int (&jl)[NB], float (&v)[NB]) {
     const float* tp = theta + (size_t)(unsigned)col * (size_t)f;
 #pragma unroll
-    for (int I = 0; I < NB; ++I) {
-        const int j = 16 * I + c;
-        float t = 0.f;
-        if (ok && (I < NB - 1 || j < f)) t = tp[j];
-        v[I] = t;
+    for (int I = 0; I < NB; ++I) v[I] = tp[jl[I]];
+}
+
+// Gather pipeline: steps of 4 entries run in groups of kGroup = 3; the theta loads of step
+// s + 3 are issued right after step s's operands are taken, so each gather has three steps of
+// matrix work (3 * 28 MFMAs at f = 100) of this wave to hide behind.  The group is unrolled so
+// the three in-flight buffers rotate by renaming rather than by copying registers that are still
+// loading.  Column indices and ratings come in batches of 4 groups = 48 entries through a
+// two-slot LDS ring: batch k+1 is loaded (one entry per lane) at the top of batch k's first
+// group and stored to the ring at the top of its second group, so any register carried around
+// the loop only ever waits on a load older than the gathers in flight.
+constexpr int kGroup = 3;
+constexpr int kBatchGroups = 4;
+constexpr int kBatch = 4 * kGroup * kBatchGroups;   // 48 entries
+constexpr int kRing = 2 * kBatch;
+
+template <int NB>
+__device__ __forceinline__ void mfma_step(const float (&v)[NB], f4 (&acc)[ntiles(NB)]) {
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+        for (int J = I; J < NB; ++J)
+            acc[tu(NB, I, J)] =
+                __builtin_amdgcn_mfma_f32_16x16x4f32(v[I], v[J], acc[tu(NB, I, J)], 0, 0, 0);
+}
+
+__device__ __forceinline__ void load_batch(const int32_t* __restrict__ colidx,
+                                           const float* __restrict__ vals, int64_t kbeg,
+                                           int64_t total, int64_t first, int lane, int& col,
+                                           float& rv) {
+    col = 0;
+    rv = 0.f;
+    if (lane < kBatch && first + lane < total) {
+        col = colidx[kbeg + first + lane];
+        rv = vals[kbeg + first + lane];
     }
 }
 
-// Accumulate entries [kbeg, kend) of one row into acc (lower block-triangle Gram) and bacc.
+// Accumulate entries [kbeg, kend) of one row into acc (upper block-triangle of the augmented
+// Gram matrix).  ring_c, ring_r: this wave's LDS ring, kRing entries each.
 template <int NB>
 __device__ __forceinline__ void gram_accumulate(const int32_t* __restrict__ colidx,
                                                 const float* __restrict__ vals,
                                                 const float* __restrict__ theta, int f,
                                                 int64_t kbeg, int64_t kend,
-                                                f4 (&acc)[ntiles(NB)], float (&bacc)[NB],
-                                                int lane) {
+                                                f4 (&acc)[ntiles(NB)], int* ring_c,
+                                                float* ring_r, int lane) {
     if (kbeg >= kend) return;
     const int g = lane >> 4, c = lane & 15;
-    // 64 entries (16 steps) of indices per batch, one per lane; next batch prefetched
-    int64_t base = kbeg;
-    int col_b = 0;
-    float rv_b = 0.f;
-    if (base + lane < kend) { col_b = colidx[base + lane]; rv_b = vals[base + lane]; }
-    int cnt = (int)((kend - base) < 64 ? (kend - base) : 64);
-    float vn[NB];
-    float rn;
+    // block I, lane column c holds theta[16 I + c] if that is < f, the rating if it is f, else 0
+    int jl[NB];
+    bool jv[NB], jr[NB];
+#pragma unroll
+    for (int I = 0; I < NB; ++I) {
+        const int j = 16 * I + c;
+        jv[I] = (I < NB - 1) || j < f;
+        jr[I] = (I == NB - 1) && j == f;
+        jl[I] = jv[I] ? j : 0;
+    }
+    const int64_t total = kend - kbeg;
+    const int64_t nsteps = (total + 3) >> 2;
+    const int64_t ngroups = (nsteps + kGroup - 1) / kGroup;
+    // batches 0 and 1 into ring slots 0 and 1 (entries past the end: column 0, rating 0)
     {
-        const int cs = __shfl(col_b, g);
-        rn = __shfl(rv_b, g);
-        const bool ok = g < cnt;
-        if (!ok) rn = 0.f;
-        load_step<NB>(theta, f, cs, ok, c, vn);
-    }
-    while (true) {
-        const int64_t nbase = base + 64;
-        int col_n = 0;
-        float rv_n = 0.f;
-        if (nbase + lane < kend) { col_n = colidx[nbase + lane]; rv_n = vals[nbase + lane]; }
-        const int ncnt = nbase < kend ? (int)((kend - nbase) < 64 ? (kend - nbase) : 64) : 0;
-        const int nsteps = (cnt + 3) >> 2;
-        for (int s = 0; s < nsteps; ++s) {
-            float v[NB];
-#pragma unroll
-            for (int I = 0; I < NB; ++I) v[I] = vn[I];
-            const float r = rn;
-            // issue the next step's gathers before this step's matrix ops
-            if (s + 1 < nsteps) {
-                const int src = 4 * (s + 1) + g;
-                const int cs = __shfl(col_b, src);
-                rn = __shfl(rv_b, src);
-                const bool ok = src < cnt;
-                if (!ok) rn = 0.f;
-                load_step<NB>(theta, f, cs, ok, c, vn);
-            } else if (ncnt > 0) {
-                const int cs = __shfl(col_n, g);
-                rn = __shfl(rv_n, g);
-                const bool ok = g < ncnt;
-                if (!ok) rn = 0.f;
-                load_step<NB>(theta, f, cs, ok, c, vn);
-            }
-#pragma unroll
-            for (int I = 0; I < NB; ++I) bacc[I] += r * v[I];
-#pragma unroll
-            for (int I = 0; I < NB; ++I)
-#pragma unroll
-                for (int J = 0; J <= I; ++J)
-                    acc[tix(I, J)] =
-                        __builtin_amdgcn_mfma_f32_16x16x4f32(v[I], v[J], acc[tix(I, J)], 0, 0, 0);
+        int c0, c1;
+        float r0, r1;
+        load_batch(colidx, vals, kbeg, total, 0, lane, c0, r0);
+        load_batch(colidx, vals, kbeg, total, kBatch, lane, c1, r1);
+        if (lane < kBatch) {
+            ring_c[lane] = c0; ring_r[lane] = r0;
+            ring_c[kBatch + lane] = c1; ring_r[kBatch + lane] = r1;
         }
-        if (ncnt == 0) break;
-        base = nbase;
-        col_b = col_n;
-        rv_b = rv_n;
-        cnt = ncnt;
+        __syncthreads();
     }
+    float b0[NB], b1[NB], b2[NB];
+    float r0, r1, r2;
+    r0 = ring_r[0 + g];  issue_step<NB>(theta, f, ring_c[0 + g], jl, b0);
+    r1 = ring_r[4 + g];  issue_step<NB>(theta, f, ring_c[4 + g], jl, b1);
+    r2 = ring_r[8 + g];  issue_step<NB>(theta, f, ring_c[8 + g], jl, b2);
+    int nc = 0;
+    float nr = 0.f;
+    for (int64_t q = 0; q < ngroups; ++q) {
+        const int qb = (int)(q % kBatchGroups);          // group's position in its batch
+        const int64_t k = q / kBatchGroups;              // batch index
+        const int cur = (int)(k & 1) * kBatch;           // ring slot of batch k
+        const int oth = kBatch - cur;                    // ring slot of batch k+1
+        // batch k+1 goes into the ring at the top of group 1, one group after its load was
+        // issued at the top of group 0 (the store comes first in program order, so its wait
+        // never covers the gathers issued after the load)
+        if (qb == 1 && k > 0) {
+            if (lane < kBatch) { ring_c[oth + lane] = nc; ring_r[oth + lane] = nr; }
+            __syncthreads();
+        }
+        if (qb == 0 && k > 0)
+            load_batch(colidx, vals, kbeg, total, (k + 1) * kBatch, lane, nc, nr);
+        // the steps issued in this group belong to group q+1: batch k, or k+1 when qb == 3
+        const int nbase = (qb == kBatchGroups - 1) ? oth : cur + (qb + 1) * kGroup * 4;
+        const int64_t s0 = q * kGroup;
+        // sub-step J: take step s's operands from buffer B, reissue B with step s + 3, then
+        // the matrix ops of step s (a step past the row's end adds zeros)
+#define ALS_SUBSTEP(B, R, J)                                                                 \
+        {                                                                                    \
+            const bool ok = 4 * (s0 + (J)) + g < total;                                      \
+            float v[NB];                                                                     \
+            const float r = ok ? R : 0.f;                                                    \
+            _Pragma("unroll") for (int I = 0; I < NB; ++I)                                   \
+                v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? r : 0.f);                             \
+            __builtin_amdgcn_sched_barrier(0);                                               \
+            const int src = nbase + 4 * (J) + g;                                             \
+            R = ring_r[src];                                                                 \
+            issue_step<NB>(theta, f, ring_c[src], jl, B);                                    \
+            mfma_step<NB>(v, acc);                                                           \
+        }
+        ALS_SUBSTEP(b0, r0, 0)
+        ALS_SUBSTEP(b1, r1, 1)
+        ALS_SUBSTEP(b2, r2, 2)
+#undef ALS_SUBSTEP
+    }
+    __syncthreads();   // the ring is refilled by the next row
 }
 
 // ------------------------------------------------------------------ solve in registers ---
 
-// Regularise, factor A = L L^T in place (right-looking, one column per step), fold the forward
-// substitution L y = b into the factorisation, back-substitute L^T x = y, write x_u.
-// buf: this wave's LDS, lds_floats(NB) floats.
+// LDS scratch of one wave for the solve.
 template <int NB>
-__device__ __forceinline__ void solve_row(f4 (&acc)[ntiles(NB)], float (&bacc)[NB], int f,
-                                          float lam_n, float* buf, float* __restrict__ xrow,
-                                          unsigned long long* __restrict__ nonspd, int lane) {
+struct SolveLds {
+    float W[NB][256];   // W_K = L_KK^{-1} per block, column-major: W[K][16 j + i] = W_K[i][j]
+    float T[256];       // a diagonal tile, row-major
+    float y[16 * NB];   // forward-substitution result (row f of the augmented factor)
+    float x[16 * NB];   // solution, zero past f
+    float z[16];
+};
+
+// Regularise and solve, in place on the accumulator tiles (upper block-triangle of the
+// augmented matrix M = [A b; b^T .]).  Blocked right-looking Cholesky, block K = 0..NB-1:
+//  1. the diagonal tile (symmetric, so lane (g, c) holds row c, columns 4g..4g+3) goes through
+//     LDS so that every lane holds one whole row (= column) c;
+//  2. it is factored by readlane broadcasts of the pivot and of column kk of L, and its inverse
+//     W_K = L_KK^{-1} formed column by column (lane c computes column c);
+//  3. panel: D_I = W_K U_{K,I} = L_IK^T for I > K, and trailing update U_{J,I} -= D_J^T D_I for
+//     K < J <= I, each a sum of four 16x16x4 MFMAs over a permuted contraction index 4g + s,
+//     which makes the C-layout registers themselves the A/B operands (no transposes).
+// The augmented column f carries b through the same updates, so its entries become
+// y = L^{-1} b.  Back substitution x_K = W_K^T (y_K - sum_{I>K} D_{K,I} x_I) runs last block
+// first.  Only real pivots (rows < f) are factored; the last block's padding is the identity.
+// Returns false if a pivot was not positive; writes x_u (f floats) to xrow.
+template <int NB>
+__device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float lam_n,
+                                          SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
     const int g = lane >> 4, c = lane & 15;
-    constexpr int BS = 16 * NB + 4;
-    constexpr int PIV = 16 * NB;
-    float bcol[NB];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) {   // sum b over the four 16-lane groups
-        float t = bacc[I];
-        t += __shfl_xor(t, 16);
-        t += __shfl_xor(t, 32);
-        bcol[I] = t;
-    }
+    const int nlast = f - 16 * (NB - 1);   // real columns of the last block; b is its column nlast
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-            if (c == 4 * g + r && 16 * I + c < f) acc[tix(I, I)][r] += lam_n;
+            if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] += lam_n;
 
     bool ok = true;
 #pragma unroll
     for (int K = 0; K < NB; ++K) {
-        const int kn = (f - 16 * K) < 16 ? (f - 16 * K) : 16;
-        for (int kc = 0; kc < kn; ++kc) {
-            const int k = 16 * K + kc;
-            float* b = buf + (k & 1) * BS;
-            if (c == kc) {   // the four lanes holding column k publish it (rows <= k as 0)
+        const int npiv = (K < NB - 1) ? 16 : nlast;
+        // 1. diagonal tile -> one full row per lane
+        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
+        __syncthreads();
+        float t[16];
 #pragma unroll
-                for (int I = K; I < NB; ++I) {
-                    const f4 v = acc[tix(I, K)];
-                    const int i0 = 16 * I + 4 * g;
-                    f4 w;
+        for (int q = 0; q < 4; ++q) {
+            const f4 v = *reinterpret_cast<const f4*>(&S.T[c * 16 + 4 * q]);
+            t[4 * q] = v[0]; t[4 * q + 1] = v[1]; t[4 * q + 2] = v[2]; t[4 * q + 3] = v[3];
+        }
+        // 2a. factor: lane c ends with row c of L_KK in lr[]
+        float lr[16];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) w[r] = (i0 + r > k) ? v[r] : 0.f;
-                    *reinterpret_cast<f4*>(b + i0) = w;
-                    if (I == K) {
+        for (int kk = 0; kk < 16; ++kk) {
+            if (kk < npiv) {
+                const float piv = readlane_f(t[kk], kk);
+                ok = ok && (piv > 0.f);
+                const float s = __builtin_amdgcn_rsqf(piv);
+                const float l = (c >= kk) ? t[kk] * s : 0.f;   // L[c][kk] (t is symmetric)
+                lr[kk] = l;
 #pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            if (i0 + r == k) b[PIV] = v[r];
-                    }
-                }
-            }
-            __syncthreads();
-            const float d = b[PIV];
-            ok = ok && (d > 0.f);
-            const float s = 1.0f / sqrtf(d);
-            const float yk = readlane_f(bcol[K], kc) * s;
-            f4 colv[NB];
-            float colj[NB];
-#pragma unroll
-            for (int I = K; I < NB; ++I) {
-                colv[I] = *reinterpret_cast<const f4*>(b + 16 * I + 4 * g) * s;
-                colj[I] = b[16 * I + c] * s;
-            }
-#pragma unroll
-            for (int I = K; I < NB; ++I)
-#pragma unroll
-                for (int J = K; J <= I; ++J) acc[tix(I, J)] -= colv[I] * colj[J];
-#pragma unroll
-            for (int J = K; J < NB; ++J) bcol[J] -= colj[J] * yk;
-            if (c == kc) {
-#pragma unroll
-                for (int I = K; I < NB; ++I) {
-                    const int i0 = 16 * I + 4 * g;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        if (i0 + r > k) acc[tix(I, K)][r] = colv[I][r];
-                        else if (i0 + r == k) acc[tix(I, K)][r] = d * s;
-                    }
-                }
-                bcol[K] = yk;
+                for (int i = kk + 1; i < 16; ++i) t[i] -= readlane_f(l, i) * l;
+            } else {
+                lr[kk] = (c == kk) ? 1.f : 0.f;
             }
         }
-    }
-    // back substitution L^T x = y, y held in bcol (column layout)
-    float xcol[NB];
+        if (K == NB - 1 && g == 0 && c == nlast) {   // row f of the augmented factor: y
 #pragma unroll
-    for (int J = 0; J < NB; ++J) xcol[J] = 0.f;
+            for (int kk = 0; kk < 16; ++kk)
+                if (kk < nlast) S.y[16 * K + kk] = lr[kk];
+        }
+        // 2b. W_K = L_KK^{-1}: lane c forms column c by forward substitution
+        float w[16];
 #pragma unroll
-    for (int J = NB - 1; J >= 0; --J) {
-        const int jn = (f - 16 * J) < 16 ? (f - 16 * J) : 16;
-        for (int jc = jn - 1; jc >= 0; --jc) {
-            const int j = 16 * J + jc;
-            float* b = buf + (j & 1) * BS;
-            if (g == (jc >> 2)) {   // row j of L: lanes of group jc/4, element jc%4
+        for (int i = 0; i < 16; ++i) {
+            float a = (i == c) ? 1.f : 0.f;
 #pragma unroll
-                for (int I = 0; I <= J; ++I) {
-                    const int i = 16 * I + c;
-                    const float v = pick4(acc[tix(J, I)], jc & 3);
-                    b[i] = (i <= j) ? v : 0.f;
-                }
+            for (int p = 0; p < i; ++p) a -= readlane_f(lr[p], i) * w[p];
+            w[i] = a * __builtin_amdgcn_rcpf(readlane_f(lr[i], i));
+        }
+        if (g == 0) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * q]) =
+                    f4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
+        }
+        __syncthreads();
+        if (K < NB - 1) {
+            f4 wop;   // lane (g, c), element s: W_K[c][4g + s]
+#pragma unroll
+            for (int s = 0; s < 4; ++s) wop[s] = S.W[K][(4 * g + s) * 16 + c];
+            // 3a. panel D_I = W_K U_{K,I}
+#pragma unroll
+            for (int I = K + 1; I < NB; ++I) {
+                f4 d = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    d = __builtin_amdgcn_mfma_f32_16x16x4f32(wop[s], acc[tu(NB, K, I)][s], d,
+                                                             0, 0, 0);
+                acc[tu(NB, K, I)] = d;
             }
-            __syncthreads();
-            const float xj = readlane_f(bcol[J], jc) / b[j];
+            // y_K sits in the augmented column of the last panel tile
+            if (c == nlast)
+                *reinterpret_cast<f4*>(&S.y[16 * K + 4 * g]) = acc[tu(NB, K, NB - 1)];
+            // 3b. trailing update U_{J,I} -= D_J^T D_I
 #pragma unroll
-            for (int I = 0; I <= J; ++I) {
-                const float lji = b[16 * I + c];
-                if (16 * I + c < j) bcol[I] -= lji * xj;
-            }
-            if (c == jc) xcol[J] = xj;
+            for (int J = K + 1; J < NB; ++J)
+#pragma unroll
+                for (int I = J; I < NB; ++I)
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        acc[tu(NB, J, I)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            -acc[tu(NB, K, J)][s], acc[tu(NB, K, I)][s], acc[tu(NB, J, I)], 0,
+                            0, 0);
         }
     }
-    if (g == 0) {
+    // back substitution, last block first; x is zero past f (b column and padding)
+    for (int j = lane; j < 16 * NB; j += kWave) S.x[j] = 0.f;
+    __syncthreads();
 #pragma unroll
-        for (int J = 0; J < NB; ++J)
-            if (16 * J + c < f) xrow[16 * J + c] = ok ? xcol[J] : __builtin_nanf("");
+    for (int K = NB - 1; K >= 0; --K) {
+        f4 part = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int I = K + 1; I < NB; ++I) part += acc[tu(NB, K, I)] * S.x[16 * I + c];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float v = part[r];
+            v += __shfl_xor(v, 8);
+            v += __shfl_xor(v, 4);
+            v += __shfl_xor(v, 2);
+            v += __shfl_xor(v, 1);
+            part[r] = v;
+        }
+        f4 z;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int kk = 4 * g + r;
+            z[r] = (K < NB - 1 || kk < nlast) ? S.y[16 * K + kk] - part[r] : 0.f;
+        }
+        if (c == 0) *reinterpret_cast<f4*>(&S.z[4 * g]) = z;
+        __syncthreads();
+        const float zc = S.z[c];
+        f4 xs;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) xs[s] = S.W[K][(4 * g + s) * 16 + c] * zc;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float v = xs[s];
+            v += __shfl_xor(v, 8);
+            v += __shfl_xor(v, 4);
+            v += __shfl_xor(v, 2);
+            v += __shfl_xor(v, 1);
+            xs[s] = (K < NB - 1 || 4 * g + s < nlast) ? v : 0.f;
+        }
+        if (c == 0) *reinterpret_cast<f4*>(&S.x[16 * K + 4 * g]) = xs;
+        __syncthreads();
     }
-    if (!ok && lane == 0) atomicAdd(nonspd, 1ull);
+    for (int j = lane; j < f; j += kWave) xrow[j] = ok ? S.x[j] : __builtin_nanf("");
+    return ok;
 }
 
 template <int NB>
@@ -293,25 +382,21 @@ __device__ __forceinline__ void write_zero_row(float* __restrict__ xrow, int f, 
 }
 
 template <int NB>
-__device__ __forceinline__ void store_slot(const f4 (&acc)[ntiles(NB)], const float (&bacc)[NB],
-                                           float* __restrict__ slot, int lane) {
+__device__ __forceinline__ void store_slot(const f4 (&acc)[ntiles(NB)], float* __restrict__ slot,
+                                           int lane) {
 #pragma unroll
     for (int t = 0; t < ntiles(NB); ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r) slot[(t * 4 + r) * kWave + lane] = acc[t][r];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) slot[(ntiles(NB) * 4 + I) * kWave + lane] = bacc[I];
 }
 
 template <int NB>
-__device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], float (&bacc)[NB],
-                                         const float* __restrict__ slot, int lane) {
+__device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], const float* __restrict__ slot,
+                                         int lane) {
 #pragma unroll
     for (int t = 0; t < ntiles(NB); ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[t][r] += slot[(t * 4 + r) * kWave + lane];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) bacc[I] += slot[(ntiles(NB) * 4 + I) * kWave + lane];
 }
 
 // ------------------------------------------------------------------------ kernels --------
@@ -324,7 +409,9 @@ __global__ __launch_bounds__(kWave) void k_herm_solve(
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int f,
     float lambda, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
     float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
-    __shared__ __attribute__((aligned(16))) float buf[lds_floats(NB)];
+    __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
+    __shared__ int ring_c[kRing];
+    __shared__ float ring_r[kRing];
     const int lane = threadIdx.x;
     const int w = blockIdx.x;
     const int64_t u0 = bounds[2 * w], k0 = bounds[2 * w + 1];
@@ -343,18 +430,16 @@ __global__ __launch_bounds__(kWave) void k_herm_solve(
         }
         if (ka >= kb) continue;              // nothing of this row in the share
         f4 acc[ntiles(NB)];
-        float bacc[NB];
 #pragma unroll
         for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int I = 0; I < NB; ++I) bacc[I] = 0.f;
-        gram_accumulate<NB>(colidx, vals, theta, f, rs + ka, rs + kb, acc, bacc, lane);
+        gram_accumulate<NB>(colidx, vals, theta, f, rs + ka, rs + kb, acc, ring_c, ring_r, lane);
         if (ka == 0 && kb == nu) {
             const float lam_n = (float)((double)lambda * (double)nu);
-            solve_row<NB>(acc, bacc, f, lam_n, buf, x_out + (size_t)u * f, nonspd, lane);
+            if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane) && lane == 0)
+                atomicAdd(nonspd, 1ull);
         } else {
             const int which = (u == u0) ? 0 : 1;
-            store_slot<NB>(acc, bacc, slots + (size_t)(2 * w + which) * slot_floats(NB), lane);
+            store_slot<NB>(acc, slots + (size_t)(2 * w + which) * slot_floats(NB), lane);
         }
     }
 }
@@ -366,7 +451,7 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
     const int64_t* __restrict__ rowptr, int64_t m, int W, int f, float lambda,
     const int64_t* __restrict__ bounds, float* __restrict__ x_out,
     const float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
-    __shared__ __attribute__((aligned(16))) float buf[lds_floats(NB)];
+    __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
     const int lane = threadIdx.x;
     const int b = blockIdx.x + 1;
     if (b >= W) return;
@@ -378,15 +463,12 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
     const int64_t u = bounds[2 * b];
     if (b > 1 && cuts(b - 1) && bounds[2 * (b - 1)] == u) return;   // not the first cut
     f4 acc[ntiles(NB)];
-    float bacc[NB];
 #pragma unroll
     for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int I = 0; I < NB; ++I) bacc[I] = 0.f;
     // wave b-1 holds the row's first piece: as its first piece if it started in row u
     // (then at entry 0), else as its last piece
     const int first_slot = (bounds[2 * (b - 1)] == u) ? 2 * (b - 1) : 2 * (b - 1) + 1;
-    add_slot<NB>(acc, bacc, slots + (size_t)first_slot * slot_floats(NB), lane);
+    add_slot<NB>(acc, slots + (size_t)first_slot * slot_floats(NB), lane);
     const int64_t nu = rowptr[u + 1] - rowptr[u];
     for (int bb = b;; ++bb) {   // waves b, b+1, ... start inside row u: their first piece
         const bool more = bb + 1 < W && cuts(bb + 1) && bounds[2 * (bb + 1)] == u;
@@ -394,11 +476,12 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
         // piece of row u and wrote no slot
         const int64_t piece_end = more ? bounds[2 * (bb + 1) + 1] : nu;
         if (bounds[2 * bb + 1] < piece_end)
-            add_slot<NB>(acc, bacc, slots + (size_t)(2 * bb) * slot_floats(NB), lane);
+            add_slot<NB>(acc, slots + (size_t)(2 * bb) * slot_floats(NB), lane);
         if (!more) break;
     }
     const float lam_n = (float)((double)lambda * (double)nu);
-    solve_row<NB>(acc, bacc, f, lam_n, buf, x_out + (size_t)u * f, nonspd, lane);
+    if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane) && lane == 0)
+        atomicAdd(nonspd, 1ull);
 }
 
 // RMSE: wave w covers entries [nnz w / W, nnz (w+1) / W); each 16-lane group takes one entry
@@ -512,26 +595,26 @@ int waves_for_nb(int nb, int cus, int* w) {
         case 6: return occupancy_waves<6>(cus, w);
         case 7: return occupancy_waves<7>(cus, w);
         case 8: return occupancy_waves<8>(cus, w);
+        case 9: return occupancy_waves<9>(cus, w);
         default: return -1;
     }
 }
 
-int nb_of(int f) { return (f + 15) / 16; }
+int nb_of(int f) { return f / 16 + 1; }   // blocks of 16 covering the augmented f + 1
 
-// Solve cost of one row in c_nnz units: the Cholesky runs on the vector ALU while other waves
-// keep the matrix cores busy, so it is charged at a fraction of its latency.  Tunable through
-// ALS_ROW_COST (entries per row).
+// Solve cost of one row in c_nnz units: per 16-column block about 2,500 cycles of factor and
+// inverse on the vector ALU plus the panel and trailing-update MFMAs (32 cycles each); the
+// vector part overlaps other waves' matrix work, so half of the total is charged.  Tunable
+// through ALS_ROW_COST (entries per row).
 int64_t row_cost(int f) {
     const char* env = getenv("ALS_ROW_COST");
     if (env && atoll(env) > 0) return atoll(env) * kCostPerEntry;
     const int nb = nb_of(f);
     const double mfma_cycles_per_entry = 8.0 * ntiles(nb);
-    const double chol_cycles = 16.0 * 4.0 * 4.0 * [&] {
-        double t = 0;
-        for (int K = 0; K < nb; ++K) t += (nb - K) * (nb - K + 1) / 2.0;
-        return t;
-    }() + 60.0 * f;
-    double entries = 0.5 * chol_cycles / mfma_cycles_per_entry;
+    double mfmas = 0;
+    for (int K = 0; K < nb; ++K) mfmas += 4.0 * ((nb - K - 1) + (nb - K - 1) * (nb - K) / 2.0);
+    const double solve_cycles = 2500.0 * nb + 32.0 * mfmas;
+    double entries = 0.5 * solve_cycles / mfma_cycles_per_entry;
     if (entries < 1.0) entries = 1.0;
     return (int64_t)(entries * kCostPerEntry);
 }
@@ -747,6 +830,7 @@ int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
         case 6: launch_sweep<6>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
         case 7: launch_sweep<7>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
         case 8: launch_sweep<8>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
+        case 9: launch_sweep<9>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
         default: return ALS_ERR_UNSUPPORTED_F;
     }
     hipError_t e = hipGetLastError();
