@@ -44,6 +44,7 @@ constexpr int kMaxNB = ALS_F_MAX / 16 + 1;      // 9 column blocks of 16 cover f
 constexpr int kSnap = 256;                      // partition cut grid (entries)
 constexpr int kCostPerEntry = 16;               // c_nnz
 constexpr int kMaxWavesPerCU = 32;
+constexpr int kRmseWavesPerCU = 24;                // RMSE: 6 waves per SIMD, latency hiding
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
 // upper block-triangle, row-major: tile (I, J) with I <= J
@@ -53,6 +54,22 @@ constexpr int slot_floats(int nb) { return ntiles(nb) * 4 * kWave; }
 
 __device__ __forceinline__ float readlane_f(float v, int lane) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 16 lanes of a DPP row (lanes 16g..16g+15), returned to all 16 lanes with the
+// same bits: swap neighbours, swap pairs (quad_perm), then mirror within 8 and within 16.
+__device__ __forceinline__ float row_sum16(float v) {
+    v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+    v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dpp_f<0x141>(v);   // row_half_mirror
+    v += dpp_f<0x140>(v);   // row_mirror
+    return v;
 }
 
 // ------------------------------------------------------------------------------- plan ----
@@ -228,19 +245,151 @@ struct SolveLds {
     float z[16];
 };
 
+// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major).  Lane c
+// keeps column c of the Schur complement in t[] and column c of W_K = L_KK^{-1} in w[] (from
+// e_c): step kk broadcasts the pivot and column kk of L by readlane, which is also what the row
+// operations of L W = I need.  npiv real pivots; the rest of the tile is the identity.  In the
+// last block the row nlast is the augmented b row, whose L entries are y (written to S.y).
+template <int NB>
+__device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, int nlast,
+                                            bool& ok, int lane) {
+    const int g = lane >> 4, c = lane & 15;
+    float t[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const f4 v = *reinterpret_cast<const f4*>(&S.T[c * 16 + 4 * q]);
+        t[4 * q] = v[0]; t[4 * q + 1] = v[1]; t[4 * q + 2] = v[2]; t[4 * q + 3] = v[3];
+    }
+    const bool y_lane = (K == NB - 1) && g == 0 && c == nlast;
+    float w[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) w[i] = (i == c) ? 1.f : 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+        if (kk < npiv) {
+            const float piv = readlane_f(t[kk], kk);
+            ok = ok && (piv > 0.f);
+            const float s = __builtin_amdgcn_rsqf(piv);
+            const float l = (c >= kk) ? t[kk] * s : 0.f;   // L[c][kk] (t is symmetric)
+            if (y_lane) S.y[16 * K + kk] = l;
+            w[kk] *= s;
+#pragma unroll
+            for (int i = kk + 1; i < 16; ++i) {
+                const float li = readlane_f(l, i);
+                t[i] -= li * l;
+                w[i] -= li * w[kk];
+            }
+        }
+    }
+    if (g == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * q]) =
+                f4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
+    }
+}
+
+// Block K's acc-indexed steps, one instantiation per K (the block loop runs at run time so the
+// factor code above exists once):
+//   stage: diagonal tile -> S.T, so that lane c can read row (= column) c;
+//   panel: D_I = W_K U_{K,I} = L_IK^T for I > K; y_K from the augmented column; trailing update
+//          U_{J,I} -= D_J^T D_I for K < J <= I.  Each product is four 16x16x4 MFMAs over the
+//          permuted contraction index p = 4g + s, under which lane (g, c) element s of a C-layout
+//          tile is both the A operand (of its transpose) and the B operand;
+//   matvec: sum_{I>K} D_{K,I}[4g + r][c] x[16 I + c] per lane (summed over c by the caller).
+template <int NB, int K>
+struct Block {
+    static __device__ __forceinline__ void stage(const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
+                                                 int lane) {
+        const int g = lane >> 4, c = lane & 15;
+        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
+    }
+    static __device__ __forceinline__ void panel(f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
+                                                 int nlast, int lane) {
+        if constexpr (K < NB - 1) {
+            const int g = lane >> 4, c = lane & 15;
+            f4 wop;   // element s: W_K[c][4g + s]
+#pragma unroll
+            for (int s = 0; s < 4; ++s) wop[s] = S.W[K][(4 * g + s) * 16 + c];
+#pragma unroll
+            for (int I = K + 1; I < NB; ++I) {
+                f4 d = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    d = __builtin_amdgcn_mfma_f32_16x16x4f32(wop[s], acc[tu(NB, K, I)][s], d,
+                                                             0, 0, 0);
+                acc[tu(NB, K, I)] = d;
+            }
+            if (c == nlast)   // y_K: the augmented column of the last panel tile
+                *reinterpret_cast<f4*>(&S.y[16 * K + 4 * g]) = acc[tu(NB, K, NB - 1)];
+#pragma unroll
+            for (int J = K + 1; J < NB; ++J)
+#pragma unroll
+                for (int I = J; I < NB; ++I)
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        acc[tu(NB, J, I)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            -acc[tu(NB, K, J)][s], acc[tu(NB, K, I)][s], acc[tu(NB, J, I)], 0,
+                            0, 0);
+        }
+    }
+    static __device__ __forceinline__ f4 matvec(const f4 (&acc)[ntiles(NB)],
+                                                const SolveLds<NB>& S, int lane) {
+        const int c = lane & 15;
+        f4 part = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int I = K + 1; I < NB; ++I) part += acc[tu(NB, K, I)] * S.x[16 * I + c];
+        return part;
+    }
+};
+
+// run-time K -> Block<NB, K>
+// run-time K -> Block<NB, K>.  Each case ends in its own empty asm statement so that the
+// optimiser cannot merge the cases into one access with a run-time tile index (which would move
+// the accumulator tiles out of registers).
+template <int K>
+__device__ __forceinline__ void case_marker() {
+    asm volatile("; als block case %0" ::"n"(K));
+}
+template <int NB, int K = 0>
+__device__ __forceinline__ void stage_diag(int k, const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
+                                           int lane) {
+    if (k == K) {
+        Block<NB, K>::stage(acc, S, lane);
+        case_marker<K>();
+    } else if constexpr (K + 1 < NB) {
+        stage_diag<NB, K + 1>(k, acc, S, lane);
+    }
+}
+template <int NB, int K = 0>
+__device__ __forceinline__ void panel_update(int k, f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
+                                             int nlast, int lane) {
+    if (k == K) {
+        Block<NB, K>::panel(acc, S, nlast, lane);
+        case_marker<K>();
+    } else if constexpr (K + 1 < NB - 1) {
+        panel_update<NB, K + 1>(k, acc, S, nlast, lane);
+    }
+}
+template <int NB, int K = 0>
+__device__ __forceinline__ f4 back_matvec(int k, const f4 (&acc)[ntiles(NB)],
+                                          const SolveLds<NB>& S, int lane) {
+    if (k == K) {
+        const f4 r = Block<NB, K>::matvec(acc, S, lane);
+        case_marker<K>();
+        return r;
+    }
+    if constexpr (K + 1 < NB) return back_matvec<NB, K + 1>(k, acc, S, lane);
+    return f4{0.f, 0.f, 0.f, 0.f};
+}
+
 // Regularise and solve, in place on the accumulator tiles (upper block-triangle of the
-// augmented matrix M = [A b; b^T .]).  Blocked right-looking Cholesky, block K = 0..NB-1:
-//  1. the diagonal tile (symmetric, so lane (g, c) holds row c, columns 4g..4g+3) goes through
-//     LDS so that every lane holds one whole row (= column) c;
-//  2. it is factored by readlane broadcasts of the pivot and of column kk of L, and its inverse
-//     W_K = L_KK^{-1} formed column by column (lane c computes column c);
-//  3. panel: D_I = W_K U_{K,I} = L_IK^T for I > K, and trailing update U_{J,I} -= D_J^T D_I for
-//     K < J <= I, each a sum of four 16x16x4 MFMAs over a permuted contraction index 4g + s,
-//     which makes the C-layout registers themselves the A/B operands (no transposes).
-// The augmented column f carries b through the same updates, so its entries become
-// y = L^{-1} b.  Back substitution x_K = W_K^T (y_K - sum_{I>K} D_{K,I} x_I) runs last block
-// first.  Only real pivots (rows < f) are factored; the last block's padding is the identity.
-// Returns false if a pivot was not positive; writes x_u (f floats) to xrow.
+// augmented matrix M = [A b; b^T .]).  Blocked right-looking Cholesky over the 16-column blocks:
+// factor and invert the diagonal tile (factor_tile), then panel and trailing update by MFMA
+// (Block::panel).  The augmented column carries b through the same updates, so its entries
+// become y = L^{-1} b.  Back substitution x_K = W_K^T (y_K - sum_{I>K} D_{K,I} x_I) runs last
+// block first.  Only real pivots (rows < f) are factored; the last block's padding is the
+// identity.  Returns false if a pivot was not positive; writes x_u (f floats) to xrow.
 template <int NB>
 __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float lam_n,
                                           SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
@@ -253,101 +402,22 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
             if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] += lam_n;
 
     bool ok = true;
-#pragma unroll
+#pragma unroll 1
     for (int K = 0; K < NB; ++K) {
-        const int npiv = (K < NB - 1) ? 16 : nlast;
-        // 1. diagonal tile -> one full row per lane
-        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
+        stage_diag<NB>(K, acc, S, lane);
         __syncthreads();
-        float t[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const f4 v = *reinterpret_cast<const f4*>(&S.T[c * 16 + 4 * q]);
-            t[4 * q] = v[0]; t[4 * q + 1] = v[1]; t[4 * q + 2] = v[2]; t[4 * q + 3] = v[3];
-        }
-        // 2a. factor: lane c ends with row c of L_KK in lr[]
-        float lr[16];
-#pragma unroll
-        for (int kk = 0; kk < 16; ++kk) {
-            if (kk < npiv) {
-                const float piv = readlane_f(t[kk], kk);
-                ok = ok && (piv > 0.f);
-                const float s = __builtin_amdgcn_rsqf(piv);
-                const float l = (c >= kk) ? t[kk] * s : 0.f;   // L[c][kk] (t is symmetric)
-                lr[kk] = l;
-#pragma unroll
-                for (int i = kk + 1; i < 16; ++i) t[i] -= readlane_f(l, i) * l;
-            } else {
-                lr[kk] = (c == kk) ? 1.f : 0.f;
-            }
-        }
-        if (K == NB - 1 && g == 0 && c == nlast) {   // row f of the augmented factor: y
-#pragma unroll
-            for (int kk = 0; kk < 16; ++kk)
-                if (kk < nlast) S.y[16 * K + kk] = lr[kk];
-        }
-        // 2b. W_K = L_KK^{-1}: lane c forms column c by forward substitution
-        float w[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            float a = (i == c) ? 1.f : 0.f;
-#pragma unroll
-            for (int p = 0; p < i; ++p) a -= readlane_f(lr[p], i) * w[p];
-            w[i] = a * __builtin_amdgcn_rcpf(readlane_f(lr[i], i));
-        }
-        if (g == 0) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * q]) =
-                    f4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
-        }
+        factor_tile<NB>(S, K, (K < NB - 1) ? 16 : nlast, nlast, ok, lane);
         __syncthreads();
-        if (K < NB - 1) {
-            f4 wop;   // lane (g, c), element s: W_K[c][4g + s]
-#pragma unroll
-            for (int s = 0; s < 4; ++s) wop[s] = S.W[K][(4 * g + s) * 16 + c];
-            // 3a. panel D_I = W_K U_{K,I}
-#pragma unroll
-            for (int I = K + 1; I < NB; ++I) {
-                f4 d = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    d = __builtin_amdgcn_mfma_f32_16x16x4f32(wop[s], acc[tu(NB, K, I)][s], d,
-                                                             0, 0, 0);
-                acc[tu(NB, K, I)] = d;
-            }
-            // y_K sits in the augmented column of the last panel tile
-            if (c == nlast)
-                *reinterpret_cast<f4*>(&S.y[16 * K + 4 * g]) = acc[tu(NB, K, NB - 1)];
-            // 3b. trailing update U_{J,I} -= D_J^T D_I
-#pragma unroll
-            for (int J = K + 1; J < NB; ++J)
-#pragma unroll
-                for (int I = J; I < NB; ++I)
-#pragma unroll
-                    for (int s = 0; s < 4; ++s)
-                        acc[tu(NB, J, I)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            -acc[tu(NB, K, J)][s], acc[tu(NB, K, I)][s], acc[tu(NB, J, I)], 0,
-                            0, 0);
-        }
+        panel_update<NB>(K, acc, S, nlast, lane);
     }
     // back substitution, last block first; x is zero past f (b column and padding)
     for (int j = lane; j < 16 * NB; j += kWave) S.x[j] = 0.f;
     __syncthreads();
-#pragma unroll
+#pragma unroll 1
     for (int K = NB - 1; K >= 0; --K) {
-        f4 part = f4{0.f, 0.f, 0.f, 0.f};
+        f4 part = back_matvec<NB>(K, acc, S, lane);
 #pragma unroll
-        for (int I = K + 1; I < NB; ++I) part += acc[tu(NB, K, I)] * S.x[16 * I + c];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float v = part[r];
-            v += __shfl_xor(v, 8);
-            v += __shfl_xor(v, 4);
-            v += __shfl_xor(v, 2);
-            v += __shfl_xor(v, 1);
-            part[r] = v;
-        }
+        for (int r = 0; r < 4; ++r) part[r] = row_sum16(part[r]);
         f4 z;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -362,11 +432,7 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
         for (int s = 0; s < 4; ++s) xs[s] = S.W[K][(4 * g + s) * 16 + c] * zc;
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            float v = xs[s];
-            v += __shfl_xor(v, 8);
-            v += __shfl_xor(v, 4);
-            v += __shfl_xor(v, 2);
-            v += __shfl_xor(v, 1);
+            const float v = row_sum16(xs[s]);
             xs[s] = (K < NB - 1 || 4 * g + s < nlast) ? v : 0.f;
         }
         if (c == 0) *reinterpret_cast<f4*>(&S.x[16 * K + 4 * g]) = xs;
@@ -485,11 +551,18 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
 }
 
 // RMSE: wave w covers entries [nnz w / W, nnz (w+1) / W); each 16-lane group takes one entry
-// per step.  Partial sums in fp64, one per wave.
+// per step and reads 64 contiguous bytes of theta_v and of x_u per column block, through the
+// same three-step gather pipeline as the Gram (the ring also carries each entry's row, found
+// by walking rowptr once per batch, so the pipeline runs across row boundaries).  The residual
+// is formed in fp32; squares are summed in fp64 per wave.
+template <int NB>   // NB = ceil(f / 16) column blocks
 __global__ __launch_bounds__(kWave) void k_rmse_partial(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, int64_t m, int f, const float* __restrict__ x,
     const float* __restrict__ theta, int W, double* __restrict__ partial) {
+    __shared__ int ring_c[kRing];
+    __shared__ float ring_r[kRing];
+    __shared__ int64_t ring_u[kRing];
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int w = blockIdx.x;
     const int64_t nnz = rowptr[m];
@@ -502,26 +575,93 @@ __global__ __launch_bounds__(kWave) void k_rmse_partial(
             const int64_t mid = (lo + hi + 1) >> 1;
             if (rowptr[mid] <= kb) lo = mid; else hi = mid - 1;
         }
-        int64_t u = lo;
-        for (int64_t k = kb + g; k - g < ke; k += 4) {
-            const bool ok = k < ke;
-            float part = 0.f;
-            float r = 0.f;
-            if (ok) {
+        int64_t ubatch = lo;
+        int jl[NB];
+        bool jv[NB];
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+            const int j = 16 * I + c;
+            jv[I] = j < f;
+            jl[I] = jv[I] ? j : 0;
+        }
+        const int64_t total = ke - kb;
+        const int64_t nsteps = (total + 3) >> 2;
+        const int64_t ngroups = (nsteps + kGroup - 1) / kGroup;
+        // one batch of entries: column, rating and row (entries past the end: row ubatch, col 0)
+        auto load_batch_rows = [&](int64_t first, int& col, float& rv, int64_t& u) {
+            col = 0;
+            rv = 0.f;
+            u = ubatch;
+            const int64_t k = kb + first + lane;
+            if (lane < kBatch && first + lane < total) {
+                col = colidx[k];
+                rv = vals[k];
                 while (rowptr[u + 1] <= k) ++u;
-                const float* tp = theta + (size_t)(unsigned)colidx[k] * f;
-                const float* xp = x + (size_t)u * f;
-                for (int j = c; j < f; j += 16) part += tp[j] * xp[j];
-                r = vals[k];
             }
-            part += __shfl_xor(part, 8);
-            part += __shfl_xor(part, 4);
-            part += __shfl_xor(part, 2);
-            part += __shfl_xor(part, 1);
-            if (ok && c == 0) {
-                const double e = (double)(r - part);
-                acc += e * e;
+        };
+        {
+            int c0, c1;
+            float r0, r1;
+            int64_t u0, u1;
+            load_batch_rows(0, c0, r0, u0);
+            ubatch = __shfl(u0, kBatch - 1);
+            load_batch_rows(kBatch, c1, r1, u1);
+            ubatch = __shfl(u1, kBatch - 1);
+            if (lane < kBatch) {
+                ring_c[lane] = c0; ring_r[lane] = r0; ring_u[lane] = u0;
+                ring_c[kBatch + lane] = c1; ring_r[kBatch + lane] = r1; ring_u[kBatch + lane] = u1;
             }
+            __syncthreads();
+        }
+        float t0[NB], t1[NB], t2[NB], x0[NB], x1[NB], x2[NB];
+        float r0, r1, r2;
+        auto issue = [&](int src, float (&bt)[NB], float (&bx)[NB], float& rr) {
+            const float* tp = theta + (size_t)(unsigned)ring_c[src] * (size_t)f;
+            const float* xp = x + (size_t)ring_u[src] * (size_t)f;
+            rr = ring_r[src];
+#pragma unroll
+            for (int I = 0; I < NB; ++I) { bt[I] = tp[jl[I]]; bx[I] = xp[jl[I]]; }
+        };
+        issue(0 + g, t0, x0, r0);
+        issue(4 + g, t1, x1, r1);
+        issue(8 + g, t2, x2, r2);
+        int nc = 0;
+        float nr = 0.f;
+        int64_t nu = 0;
+        for (int64_t q = 0; q < ngroups; ++q) {
+            const int qb = (int)(q % kBatchGroups);
+            const int64_t k = q / kBatchGroups;
+            const int cur = (int)(k & 1) * kBatch;
+            const int oth = kBatch - cur;
+            if (qb == 1 && k > 0) {
+                if (lane < kBatch) { ring_c[oth + lane] = nc; ring_r[oth + lane] = nr; ring_u[oth + lane] = nu; }
+                __syncthreads();
+            }
+            if (qb == 0 && k > 0) {
+                load_batch_rows((k + 1) * kBatch, nc, nr, nu);
+                ubatch = __shfl(nu, kBatch - 1);
+            }
+            const int nbase = (qb == kBatchGroups - 1) ? oth : cur + (qb + 1) * kGroup * 4;
+            const int64_t s0 = q * kGroup;
+#define ALS_RSTEP(BT, BX, R, J)                                                              \
+            {                                                                                \
+                const bool ok = 4 * (s0 + (J)) + g < total;                                  \
+                float p = 0.f;                                                               \
+                _Pragma("unroll") for (int I = 0; I < NB; ++I)                               \
+                    p += jv[I] ? BT[I] * BX[I] : 0.f;                                        \
+                const float rr = R;                                                          \
+                __builtin_amdgcn_sched_barrier(0);                                           \
+                issue(nbase + 4 * (J) + g, BT, BX, R);                                       \
+                p = row_sum16(p);                                                            \
+                if (ok && c == 0) {                                                          \
+                    const double e = (double)(rr - p);                                       \
+                    acc += e * e;                                                            \
+                }                                                                            \
+            }
+            ALS_RSTEP(t0, x0, r0, 0)
+            ALS_RSTEP(t1, x1, r1, 1)
+            ALS_RSTEP(t2, x2, r2, 2)
+#undef ALS_RSTEP
         }
     }
     acc += __shfl_xor(acc, 16);
@@ -554,7 +694,7 @@ struct Layout {
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // waves[nb] = W for f in (16 (nb-1), 16 nb]; the slot region holds 2 W partial accumulators
-Layout make_layout(const int* waves, int nb_max) {
+Layout make_layout(const int* waves, int nb_max, int cus) {
     int w_cap = 1;
     size_t slot_bytes = 0;
     for (int nb = 1; nb <= nb_max; ++nb) {
@@ -566,7 +706,7 @@ Layout make_layout(const int* waves, int nb_max) {
     size_t off = 0;
     L.status = off; off = align256(off + 256);
     L.bounds = off; off = align256(off + sizeof(int64_t) * 2 * (size_t)(w_cap + 1));
-    L.rmse = off;   off = align256(off + sizeof(double) * (size_t)w_cap);
+    L.rmse = off;   off = align256(off + sizeof(double) * (size_t)cus * kRmseWavesPerCU);
     L.slots = off;  off = align256(off + slot_bytes);
     L.total = off;
     return L;
@@ -714,7 +854,7 @@ size_t als_workspace_bytes(int device, int32_t f_max) {
     if (f_max < 1 || f_max > ALS_F_MAX) return 0;
     int cus = 0, w_cap = 0, waves[kMaxNB + 1] = {0};
     if (query_device(device, f_max, &cus, waves, &w_cap) != ALS_OK) return 0;
-    return make_layout(waves, nb_of(f_max)).total;
+    return make_layout(waves, nb_of(f_max), cus).total;
 }
 
 int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes, int32_t f_max) {
@@ -730,7 +870,7 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
     ctx->device = device;
     ctx->f_max = f_max;
     ctx->nb_max = nb_of(f_max);
-    ctx->lay = make_layout(ctx->waves, ctx->nb_max);
+    ctx->lay = make_layout(ctx->waves, ctx->nb_max, ctx->cus);
     if (workspace_bytes < ctx->lay.total) { delete ctx; return ALS_ERR_WORKSPACE; }
     ctx->ws = (unsigned char*)workspace;
     ctx->ws_bytes = workspace_bytes;
@@ -850,11 +990,21 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
     hipStream_t st = (hipStream_t)stream;
-    const int W = ctx->w_cap;
+    const int W = ctx->cus * kRmseWavesPerCU;
     double* part = (double*)(ctx->ws + ctx->lay.rmse);
-    if (m > 0)
-        hipLaunchKernelGGL(k_rmse_partial, dim3(W), dim3(kWave), 0, st, rowptr, colidx, vals, m,
-                           f, x, theta, W, part);
+    if (m > 0) {
+        switch ((f + 15) / 16) {
+#define ALS_RMSE_CASE(NBR)                                                                       \
+            case NBR:                                                                            \
+                hipLaunchKernelGGL(k_rmse_partial<NBR>, dim3(W), dim3(kWave), 0, st, rowptr,     \
+                                   colidx, vals, m, f, x, theta, W, part);                       \
+                break;
+            ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4)
+            ALS_RMSE_CASE(5) ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8)
+#undef ALS_RMSE_CASE
+            default: return ALS_ERR_UNSUPPORTED_F;
+        }
+    }
     hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? W : 0, part,
                        rmse_out);
     hipError_t e = hipGetLastError();
