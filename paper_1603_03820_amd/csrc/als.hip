@@ -62,6 +62,34 @@ __device__ __forceinline__ float dpp_f(float v) {
         float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
+// acc + a' * b, where a' is a taken from lane N of the lane's 16-lane row (DPP row_newbcast:N)
+// folded into one v_fmac.  The caller produces `a` with neg_settled below, so the two wait states
+// a DPP source needs after its last VALU write are already there.
+template <int N>
+__device__ __forceinline__ float fmac_rowbcast(float acc, float a, float b) {
+    asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+        : "+v"(acc)
+        : "v"(a), "v"(b), "n"(N));
+    return acc;
+}
+__device__ __forceinline__ float fmac_rowbcast_n(int n, float acc, float a, float b) {
+    switch (n) {   // n is a constant after unrolling
+#define ALS_FMAC_CASE(N) case N: return fmac_rowbcast<N>(acc, a, b);
+        ALS_FMAC_CASE(0) ALS_FMAC_CASE(1) ALS_FMAC_CASE(2) ALS_FMAC_CASE(3)
+        ALS_FMAC_CASE(4) ALS_FMAC_CASE(5) ALS_FMAC_CASE(6) ALS_FMAC_CASE(7)
+        ALS_FMAC_CASE(8) ALS_FMAC_CASE(9) ALS_FMAC_CASE(10) ALS_FMAC_CASE(11)
+        ALS_FMAC_CASE(12) ALS_FMAC_CASE(13) ALS_FMAC_CASE(14) ALS_FMAC_CASE(15)
+#undef ALS_FMAC_CASE
+    }
+    return acc;
+}
+// -v, followed by the two wait states that let a DPP operation read the result.
+__device__ __forceinline__ float neg_settled(float v) {
+    float r;
+    asm volatile("v_xor_b32 %0, 0x80000000, %1\n\ts_nop 1" : "=v"(r) : "v"(v));
+    return r;
+}
+
 // Sum over the 16 lanes of a DPP row (lanes 16g..16g+15), returned to all 16 lanes with the
 // same bits: swap neighbours, swap pairs (quad_perm), then mirror within 8 and within 16.
 __device__ __forceinline__ float row_sum16(float v) {
@@ -103,28 +131,18 @@ __global__ void k_plan(const int64_t* __restrict__ rowptr, int64_t m, int W, int
 
 // --------------------------------------------------------------------- Gram + RHS --------
 
-// theta values of one 4-entry step, as MFMA operands: lane (g, c) loads theta_{v_g}[16 I + c].
-// The loads are unconditional (columns past f are clamped to a valid address, lanes past the
-// row's end read row 0); masking happens when the values are consumed, so the loads stay in
-// flight across the matrix ops of earlier steps.
-template <int NB>
-__device__ __forceinline__ void issue_step(const float* __restrict__ theta, int f, int col,
-                                           const int (&jl)[NB], float (&v)[NB]) {
-    const float* tp = theta + (size_t)(unsigned)col * (size_t)f;
-#pragma unroll
-    for (int I = 0; I < NB; ++I) v[I] = tp[jl[I]];
-}
-
-// Gather pipeline: steps of 4 entries run in groups of kGroup = 3; the theta loads of step
-// s + 3 are issued right after step s's operands are taken, so each gather has three steps of
-// matrix work (3 * 28 MFMAs at f = 100) of this wave to hide behind.  The group is unrolled so
-// the three in-flight buffers rotate by renaming rather than by copying registers that are still
-// loading.  Column indices and ratings come in batches of 4 groups = 48 entries through a
-// two-slot LDS ring: batch k+1 is loaded (one entry per lane) at the top of batch k's first
-// group and stored to the ring at the top of its second group, so any register carried around
-// the loop only ever waits on a load older than the gathers in flight.
-constexpr int kGroup = 3;
-constexpr int kBatchGroups = 4;
+// Gather pipeline: steps of 4 entries run in groups of kGroup = 4 steps with four operand
+// buffers; at sub-step J the theta loads of step s + 3 are issued into the buffer whose matrix
+// ops were issued at sub-step J - 1, then step s's own matrix ops run.  Every gather thus has
+// three steps of matrix work (3 * 28 MFMAs at f = 100) of this wave to hide behind, and the
+// unrolled group rotates the buffers by renaming, never by copying registers that are loading.
+// Each entry's gather word and rating come in batches of 3 groups = 48 entries through a
+// two-slot LDS ring (entry p of the piece sits at p mod 96): batch k+1 is loaded (one entry per
+// lane) at the top of batch k's first group and stored at the top of its second group, one group
+// before its first use, so any register carried around the loop only ever waits on a load older
+// than the gathers in flight.
+constexpr int kGroup = 4;
+constexpr int kBatchGroups = 3;
 constexpr int kBatch = 4 * kGroup * kBatchGroups;   // 48 entries
 constexpr int kRing = 2 * kBatch;
 
@@ -138,99 +156,200 @@ __device__ __forceinline__ void mfma_step(const float (&v)[NB], f4 (&acc)[ntiles
                 __builtin_amdgcn_mfma_f32_16x16x4f32(v[I], v[J], acc[tu(NB, I, J)], 0, 0, 0);
 }
 
-__device__ __forceinline__ void load_batch(const int32_t* __restrict__ colidx,
-                                           const float* __restrict__ vals, int64_t kbeg,
-                                           int64_t total, int64_t first, int lane, int& col,
-                                           float& rv) {
-    col = 0;
-    rv = 0.f;
-    if (lane < kBatch && first + lane < total) {
+// The theta gather of one step, as MFMA operands: lane (g, c) of block I reads
+// theta_{v_g}[16 I + c], and the lane of column f takes the rating.  Two forms:
+//   Gather<NB, true>, for theta below 2 GiB: raw buffer loads against a descriptor that bounds
+//     theta.  The gather word of an entry is its byte offset 4 f v; an entry past the piece's end
+//     gets the buffer size, and the lanes of padding columns add the size to their offset, so
+//     those loads return 0 by the hardware's range check and nothing is masked in the loop.
+//   Gather<NB, false>, for any size: 64-bit global loads; the gather word is the column index,
+//     loads are clamped to valid addresses (row 0 past the end, column 0 for padding) and the
+//     values are masked when consumed.
+// Both issue their loads unconditionally, so they stay in flight across earlier matrix ops.
+template <int NB, bool BUF>
+struct Gather;
+
+template <int NB>
+struct Gather<NB, true> {
+    static constexpr bool kMasked = false;
+    __amdgpu_buffer_rsrc_t rs;
+    unsigned fbytes, size, lo, llast;
+    bool jr;
+    __device__ __forceinline__ Gather(const float* theta, int64_t n, int f, int c) {
+        fbytes = 4u * (unsigned)f;
+        size = (unsigned)n * fbytes;
+        rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(theta), 0, (int)size,
+                                               0x00020000);
+        lo = 4u * (unsigned)c;
+        const int jlast = 16 * (NB - 1) + c;
+        llast = jlast < f ? 4u * (unsigned)jlast : size;
+        jr = jlast == f;
+    }
+    __device__ __forceinline__ int word(int col, bool valid) const {
+        return valid ? (int)((unsigned)col * fbytes) : (int)size;
+    }
+    __device__ __forceinline__ void issue(int e, float (&v)[NB]) const {
+        const unsigned base = (unsigned)e + lo;
+#pragma unroll
+        for (int I = 0; I < NB - 1; ++I)
+            v[I] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rs, base + 64u * I, 0, 0));
+        v[NB - 1] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(rs, (unsigned)e + llast, 0, 0));
+    }
+    __device__ __forceinline__ void operands(const float (&B)[NB], float r, bool,
+                                             float (&v)[NB]) const {
+#pragma unroll
+        for (int I = 0; I < NB - 1; ++I) v[I] = B[I];
+        v[NB - 1] = jr ? r : B[NB - 1];
+    }
+};
+
+template <int NB>
+struct Gather<NB, false> {
+    static constexpr bool kMasked = true;
+    const float* theta;
+    int f;
+    int jl[NB];
+    bool jv[NB], jr[NB];
+    __device__ __forceinline__ Gather(const float* th, int64_t, int f_, int c) : theta(th), f(f_) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+            const int j = 16 * I + c;
+            jv[I] = (I < NB - 1) || j < f;
+            jr[I] = (I == NB - 1) && j == f;
+            jl[I] = jv[I] ? j : 0;
+        }
+    }
+    __device__ __forceinline__ int word(int col, bool valid) const { return valid ? col : 0; }
+    __device__ __forceinline__ void issue(int e, float (&v)[NB]) const {
+        const float* tp = theta + (size_t)(unsigned)e * (size_t)f;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) v[I] = tp[jl[I]];
+    }
+    __device__ __forceinline__ void operands(const float (&B)[NB], float r, bool ok,
+                                             float (&v)[NB]) const {
+        const float rr = ok ? r : 0.f;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? rr : 0.f);
+    }
+};
+
+// One ring entry: gather word and rating.
+struct RingEntry {
+    int e;
+    float r;
+};
+
+// Entry `first + lane` of the piece starting at kbeg (lanes below kBatch; past the end: the
+// invalid gather word and rating 0).
+template <class G>
+__device__ __forceinline__ RingEntry load_entry(const G& gat, const int32_t* __restrict__ colidx,
+                                                const float* __restrict__ vals, int64_t kbeg,
+                                                int64_t total, int64_t first, int lane) {
+    const bool valid = lane < kBatch && first + lane < total;
+    int col = 0;
+    float rv = 0.f;
+    if (valid) {
         col = colidx[kbeg + first + lane];
         rv = vals[kbeg + first + lane];
     }
+    return RingEntry{gat.word(col, valid), rv};
+}
+
+// The first two index batches of a row piece, loaded ahead of time into registers.
+struct RowIndex {
+    RingEntry q0, q1;
+};
+
+// The gather pipeline's in-flight state: theta values and ratings of three steps (b0..b2 at
+// the top of a group; b3 is the fourth buffer of the rotation).
+template <int NB>
+struct Inflight {
+    float b0[NB], b1[NB], b2[NB], b3[NB];
+    float r0, r1, r2, r3;
+};
+
+template <class G>
+__device__ __forceinline__ void gram_prefetch(const G& gat, const int32_t* __restrict__ colidx,
+                                              const float* __restrict__ vals, int64_t kbeg,
+                                              int64_t kend, int lane, RowIndex& ix) {
+    ix.q0 = load_entry(gat, colidx, vals, kbeg, kend - kbeg, 0, lane);
+    ix.q1 = load_entry(gat, colidx, vals, kbeg, kend - kbeg, kBatch, lane);
+}
+
+// Put a piece's first two batches into ring slots 0 and 1 (the ring must be idle) and issue
+// the gathers of its first three steps.
+template <int NB, class G>
+__device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, RingEntry* ring,
+                                           int lane, Inflight<NB>& in) {
+    const int g = lane >> 4;
+    if (lane < kBatch) {
+        ring[lane] = ix.q0;
+        ring[kBatch + lane] = ix.q1;
+    }
+    __syncthreads();
+    RingEntry q = ring[0 + g];  in.r0 = q.r;  gat.issue(q.e, in.b0);
+    q = ring[4 + g];            in.r1 = q.r;  gat.issue(q.e, in.b1);
+    q = ring[8 + g];            in.r2 = q.r;  gat.issue(q.e, in.b2);
 }
 
 // Accumulate entries [kbeg, kend) of one row into acc (upper block-triangle of the augmented
-// Gram matrix).  ring_c, ring_r: this wave's LDS ring, kRing entries each.
-template <int NB>
-__device__ __forceinline__ void gram_accumulate(const int32_t* __restrict__ colidx,
-                                                const float* __restrict__ vals,
-                                                const float* __restrict__ theta, int f,
-                                                int64_t kbeg, int64_t kend,
-                                                f4 (&acc)[ntiles(NB)], int* ring_c,
-                                                float* ring_r, int lane) {
-    if (kbeg >= kend) return;
-    const int g = lane >> 4, c = lane & 15;
-    // block I, lane column c holds theta[16 I + c] if that is < f, the rating if it is f, else 0
-    int jl[NB];
-    bool jv[NB], jr[NB];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) {
-        const int j = 16 * I + c;
-        jv[I] = (I < NB - 1) || j < f;
-        jr[I] = (I == NB - 1) && j == f;
-        jl[I] = jv[I] ? j : 0;
-    }
-    const int64_t total = kend - kbeg;
-    const int64_t nsteps = (total + 3) >> 2;
-    const int64_t ngroups = (nsteps + kGroup - 1) / kGroup;
-    // batches 0 and 1 into ring slots 0 and 1 (entries past the end: column 0, rating 0)
-    {
-        int c0, c1;
-        float r0, r1;
-        load_batch(colidx, vals, kbeg, total, 0, lane, c0, r0);
-        load_batch(colidx, vals, kbeg, total, kBatch, lane, c1, r1);
-        if (lane < kBatch) {
-            ring_c[lane] = c0; ring_r[lane] = r0;
-            ring_c[kBatch + lane] = c1; ring_r[kBatch + lane] = r1;
-        }
-        __syncthreads();
-    }
-    float b0[NB], b1[NB], b2[NB];
-    float r0, r1, r2;
-    r0 = ring_r[0 + g];  issue_step<NB>(theta, f, ring_c[0 + g], jl, b0);
-    r1 = ring_r[4 + g];  issue_step<NB>(theta, f, ring_c[4 + g], jl, b1);
-    r2 = ring_r[8 + g];  issue_step<NB>(theta, f, ring_c[8 + g], jl, b2);
-    int nc = 0;
-    float nr = 0.f;
-    for (int64_t q = 0; q < ngroups; ++q) {
-        const int qb = (int)(q % kBatchGroups);          // group's position in its batch
-        const int64_t k = q / kBatchGroups;              // batch index
-        const int cur = (int)(k & 1) * kBatch;           // ring slot of batch k
-        const int oth = kBatch - cur;                    // ring slot of batch k+1
+// Gram matrix), starting from the state gram_stage left in the ring and in `in`.  ring: this
+// wave's LDS ring of kRing entries.  Returns with the ring idle.
+template <int NB, class G>
+__device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
+                                          const float* __restrict__ vals, int64_t kbeg,
+                                          int64_t kend, f4 (&acc)[ntiles(NB)], RingEntry* ring,
+                                          int lane, Inflight<NB>& in) {
+    const int g = lane >> 4;
+    // a row has fewer than 2^31 entries (its columns are distinct int32 indices)
+    const int total = (int)(kend - kbeg);
+    const int nsteps = (total + 3) >> 2;
+    const int ngroups = (nsteps + kGroup - 1) / kGroup;
+    RingEntry nq{0, 0.f};
+    int qb = 0, k = 0;   // group's position in its batch; batch of the group's steps
+    int rq = 12;         // ring position of the first step issued in the group: 4 (4q + 3) mod kRing
+    for (int q = 0; q < ngroups; ++q) {
         // batch k+1 goes into the ring at the top of group 1, one group after its load was
         // issued at the top of group 0 (the store comes first in program order, so its wait
-        // never covers the gathers issued after the load)
+        // never covers the gathers issued after the load); slot (k+1) & 1 last served batch
+        // k-1, whose final step was issued two groups earlier
         if (qb == 1 && k > 0) {
-            if (lane < kBatch) { ring_c[oth + lane] = nc; ring_r[oth + lane] = nr; }
+            if (lane < kBatch) ring[((k + 1) & 1) * kBatch + lane] = nq;
             __syncthreads();
         }
         if (qb == 0 && k > 0)
-            load_batch(colidx, vals, kbeg, total, (k + 1) * kBatch, lane, nc, nr);
-        // the steps issued in this group belong to group q+1: batch k, or k+1 when qb == 3
-        const int nbase = (qb == kBatchGroups - 1) ? oth : cur + (qb + 1) * kGroup * 4;
-        const int64_t s0 = q * kGroup;
-        // sub-step J: take step s's operands from buffer B, reissue B with step s + 3, then
-        // the matrix ops of step s (a step past the row's end adds zeros)
-#define ALS_SUBSTEP(B, R, J)                                                                 \
+            nq = load_entry(gat, colidx, vals, kbeg, total, (int64_t)(k + 1) * kBatch, lane);
+        const int s0 = q * kGroup;
+        // sub-step J: issue step s0 + J + 3 into buffer BN (free: its matrix ops were issued at
+        // sub-step J - 1), then the matrix ops of step s0 + J from buffer B (a step past the
+        // piece's end adds zeros)
+#define ALS_SUBSTEP(B, R, BN, RN, J)                                                         \
         {                                                                                    \
-            const bool ok = 4 * (s0 + (J)) + g < total;                                      \
             float v[NB];                                                                     \
-            const float r = ok ? R : 0.f;                                                    \
-            _Pragma("unroll") for (int I = 0; I < NB; ++I)                                   \
-                v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? r : 0.f);                             \
+            gat.operands(B, R, 4 * (s0 + (J)) + g < total, v);                               \
             __builtin_amdgcn_sched_barrier(0);                                               \
-            const int src = nbase + 4 * (J) + g;                                             \
-            R = ring_r[src];                                                                 \
-            issue_step<NB>(theta, f, ring_c[src], jl, B);                                    \
+            int pos = rq + 4 * (J);                                                          \
+            if (pos >= kRing) pos -= kRing;                                                  \
+            const RingEntry e = ring[pos + g];                                               \
+            RN = e.r;                                                                        \
+            gat.issue(e.e, BN);                                                              \
             mfma_step<NB>(v, acc);                                                           \
         }
-        ALS_SUBSTEP(b0, r0, 0)
-        ALS_SUBSTEP(b1, r1, 1)
-        ALS_SUBSTEP(b2, r2, 2)
+        ALS_SUBSTEP(in.b0, in.r0, in.b3, in.r3, 0)
+        ALS_SUBSTEP(in.b1, in.r1, in.b0, in.r0, 1)
+        ALS_SUBSTEP(in.b2, in.r2, in.b1, in.r1, 2)
+        ALS_SUBSTEP(in.b3, in.r3, in.b2, in.r2, 3)
 #undef ALS_SUBSTEP
+        rq += 4 * kGroup;
+        if (rq >= kRing) rq -= kRing;
+        if (++qb == kBatchGroups) {
+            qb = 0;
+            ++k;
+        }
     }
-    __syncthreads();   // the ring is refilled by the next row
+    __syncthreads();   // the ring is refilled by the next piece
 }
 
 // ------------------------------------------------------------------ solve in registers ---
@@ -253,7 +372,9 @@ struct SolveLds {
 template <int NB>
 __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, int nlast,
                                             bool& ok, int lane) {
-    const int g = lane >> 4, c = lane & 15;
+    const int g = lane >> 4;
+    int c = lane & 15;
+    asm volatile("" : "+v"(c));   // rebuild e_c per block rather than keep 16 registers live
     float t[16];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -273,11 +394,12 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
             const float l = (c >= kk) ? t[kk] * s : 0.f;   // L[c][kk] (t is symmetric)
             if (y_lane) S.y[16 * K + kk] = l;
             w[kk] *= s;
+            const float nl = neg_settled(l);
+            // t[i] -= L[i][kk] L[c][kk], w[i] -= L[i][kk] w[kk]; L[i][kk] is lane i's l
 #pragma unroll
             for (int i = kk + 1; i < 16; ++i) {
-                const float li = readlane_f(l, i);
-                t[i] -= li * l;
-                w[i] -= li * w[kk];
+                t[i] = fmac_rowbcast_n(i, t[i], nl, l);
+                w[i] = fmac_rowbcast_n(i, w[i], nl, w[kk]);
             }
         }
     }
@@ -291,26 +413,29 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
 
 // Block K's acc-indexed steps, one instantiation per K (the block loop runs at run time so the
 // factor code above exists once):
-//   stage: diagonal tile -> S.T, so that lane c can read row (= column) c;
-//   panel: D_I = W_K U_{K,I} = L_IK^T for I > K; y_K from the augmented column; trailing update
-//          U_{J,I} -= D_J^T D_I for K < J <= I.  Each product is four 16x16x4 MFMAs over the
-//          permuted contraction index p = 4g + s, under which lane (g, c) element s of a C-layout
-//          tile is both the A operand (of its transpose) and the B operand;
+// The tiles not yet factored hold the Schur complement negated (-U), so that the trailing update
+// is a plain multiply-accumulate.
+//   stage: diagonal tile U_KK = -acc -> S.T, so that lane c can read row (= column) c;
+//   panel: D_I = W_K U_{K,I} = L_IK^T for I > K (stored positive); y_K from the augmented
+//          column; trailing update -U_{J,I} += D_J^T D_I for K < J <= I.  Each product is four
+//          16x16x4 MFMAs over the permuted contraction index p = 4g + s, under which lane (g, c)
+//          element s of a C-layout tile is both the A operand (of its transpose) and the B
+//          operand;
 //   matvec: sum_{I>K} D_{K,I}[4g + r][c] x[16 I + c] per lane (summed over c by the caller).
 template <int NB, int K>
 struct Block {
     static __device__ __forceinline__ void stage(const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
                                                  int lane) {
         const int g = lane >> 4, c = lane & 15;
-        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
+        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = -acc[tu(NB, K, K)];
     }
     static __device__ __forceinline__ void panel(f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
                                                  int nlast, int lane) {
         if constexpr (K < NB - 1) {
             const int g = lane >> 4, c = lane & 15;
-            f4 wop;   // element s: W_K[c][4g + s]
+            f4 wop;   // element s: -W_K[c][4g + s] (the tiles hold -U)
 #pragma unroll
-            for (int s = 0; s < 4; ++s) wop[s] = S.W[K][(4 * g + s) * 16 + c];
+            for (int s = 0; s < 4; ++s) wop[s] = -S.W[K][(4 * g + s) * 16 + c];
 #pragma unroll
             for (int I = K + 1; I < NB; ++I) {
                 f4 d = f4{0.f, 0.f, 0.f, 0.f};
@@ -329,7 +454,7 @@ struct Block {
 #pragma unroll
                     for (int s = 0; s < 4; ++s)
                         acc[tu(NB, J, I)] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            -acc[tu(NB, K, J)][s], acc[tu(NB, K, I)][s], acc[tu(NB, J, I)], 0,
+                            acc[tu(NB, K, J)][s], acc[tu(NB, K, I)][s], acc[tu(NB, J, I)], 0,
                             0, 0);
         }
     }
@@ -395,11 +520,14 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
                                           SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
     const int g = lane >> 4, c = lane & 15;
     const int nlast = f - 16 * (NB - 1);   // real columns of the last block; b is its column nlast
+    // -M, regularised: the factorisation below keeps unfactored tiles negated
+#pragma unroll
+    for (int t = 0; t < ntiles(NB); ++t) acc[t] = -acc[t];
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-            if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] += lam_n;
+            if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] -= lam_n;
 
     bool ok = true;
 #pragma unroll 1
@@ -469,44 +597,77 @@ __device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], const float* __r
 
 // Wave w: entries from bounds[w] to bounds[w+1].  Whole rows are solved here; the piece of a
 // row cut at the start of the share goes to slot 2w, the piece cut at its end to slot 2w+1.
-template <int NB>
-__global__ __launch_bounds__(kWave) void k_herm_solve(
+// Rows are software-pipelined: the next piece's index batches load while this piece's Gram
+// runs, and its first theta gathers are in flight while this piece is solved.
+struct Piece {
+    int64_t u, beg, end;   // row, entry range [beg, end)
+    bool whole;            // the share holds the whole row
+};
+
+template <int NB, bool BUF>
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 7 ? 2 : 1)))
+void k_herm_solve(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
-    const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int f,
-    float lambda, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
+    const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int64_t n,
+    int f, float lambda, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
     float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
-    __shared__ int ring_c[kRing];
-    __shared__ float ring_r[kRing];
+    __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x;
     const int w = blockIdx.x;
     const int64_t u0 = bounds[2 * w], k0 = bounds[2 * w + 1];
     const int64_t u1 = bounds[2 * w + 2], k1 = bounds[2 * w + 3];
-    for (int64_t u = u0; u <= u1 && u < m; ++u) {
-        const int64_t rs = rowptr[u], nu = rowptr[u + 1] - rs;
-        const int64_t ka = (u == u0) ? k0 : 0;
-        int64_t kb = nu;
-        if (u == u1) {
-            if (k1 == 0) break;
-            kb = k1;
+    // the first piece with entries at or after row u; empty rows on the way get x_u = 0
+    auto next_piece = [&](int64_t u, Piece& p) -> bool {
+        for (; u <= u1 && u < m; ++u) {
+            const int64_t rs = rowptr[u], nu = rowptr[u + 1] - rs;
+            const int64_t ka = (u == u0) ? k0 : 0;
+            int64_t kb = nu;
+            if (u == u1) {
+                if (k1 == 0) return false;
+                kb = k1;
+            }
+            if (nu == 0) {
+                write_zero_row<NB>(x_out + (size_t)u * f, f, lane);
+                continue;
+            }
+            if (ka >= kb) continue;
+            p = Piece{u, rs + ka, rs + kb, ka == 0 && kb == nu};
+            return true;
         }
-        if (nu == 0) {                       // empty row: x_u = 0
-            write_zero_row<NB>(x_out + (size_t)u * f, f, lane);
-            continue;
-        }
-        if (ka >= kb) continue;              // nothing of this row in the share
+        return false;
+    };
+    Piece cur;
+    if (!next_piece(u0, cur)) return;
+    const Gather<NB, BUF> gat(theta, n, f, lane & 15);
+    RowIndex ix;
+    Inflight<NB> in;
+    gram_prefetch(gat, colidx, vals, cur.beg, cur.end, lane, ix);
+    gram_stage<NB>(gat, ix, ring, lane, in);
+    for (;;) {
+        Piece nxt;
+        const bool more = next_piece(cur.u + 1, nxt);
+        if (more) gram_prefetch(gat, colidx, vals, nxt.beg, nxt.end, lane, ix);
         f4 acc[ntiles(NB)];
 #pragma unroll
         for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-        gram_accumulate<NB>(colidx, vals, theta, f, rs + ka, rs + kb, acc, ring_c, ring_r, lane);
-        if (ka == 0 && kb == nu) {
+        gram_loop<NB>(gat, colidx, vals, cur.beg, cur.end, acc, ring, lane, in);
+        if (more) gram_stage<NB>(gat, ix, ring, lane, in);
+        // the solve is a latency-bound chain; raised priority lets it win issue slots over the
+        // other wave's independent Gram MFMAs, which then fill the solve's gaps
+        __builtin_amdgcn_s_setprio(2);
+        if (cur.whole) {
+            const int64_t nu = cur.end - cur.beg;
             const float lam_n = (float)((double)lambda * (double)nu);
-            if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane) && lane == 0)
+            if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)cur.u * f, lane) && lane == 0)
                 atomicAdd(nonspd, 1ull);
         } else {
-            const int which = (u == u0) ? 0 : 1;
+            const int which = (cur.u == u0) ? 0 : 1;
             store_slot<NB>(acc, slots + (size_t)(2 * w + which) * slot_floats(NB), lane);
         }
+        __builtin_amdgcn_s_setprio(0);
+        if (!more) break;
+        cur = nxt;
     }
 }
 
@@ -550,6 +711,11 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
         atomicAdd(nonspd, 1ull);
 }
 
+// RMSE pipeline shape: groups of three steps with three buffers, batches of four groups.
+constexpr int kRGroup = 3;
+constexpr int kRBatchGroups = 4;
+static_assert(4 * kRGroup * kRBatchGroups == kBatch, "RMSE batches share the ring size");
+
 // RMSE: wave w covers entries [nnz w / W, nnz (w+1) / W); each 16-lane group takes one entry
 // per step and reads 64 contiguous bytes of theta_v and of x_u per column block, through the
 // same three-step gather pipeline as the Gram (the ring also carries each entry's row, found
@@ -586,7 +752,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_partial(
         }
         const int64_t total = ke - kb;
         const int64_t nsteps = (total + 3) >> 2;
-        const int64_t ngroups = (nsteps + kGroup - 1) / kGroup;
+        const int64_t ngroups = (nsteps + kRGroup - 1) / kRGroup;
         // one batch of entries: column, rating and row (entries past the end: row ubatch, col 0)
         auto load_batch_rows = [&](int64_t first, int& col, float& rv, int64_t& u) {
             col = 0;
@@ -629,8 +795,8 @@ __global__ __launch_bounds__(kWave) void k_rmse_partial(
         float nr = 0.f;
         int64_t nu = 0;
         for (int64_t q = 0; q < ngroups; ++q) {
-            const int qb = (int)(q % kBatchGroups);
-            const int64_t k = q / kBatchGroups;
+            const int qb = (int)(q % kRBatchGroups);
+            const int64_t k = q / kRBatchGroups;
             const int cur = (int)(k & 1) * kBatch;
             const int oth = kBatch - cur;
             if (qb == 1 && k > 0) {
@@ -641,8 +807,8 @@ __global__ __launch_bounds__(kWave) void k_rmse_partial(
                 load_batch_rows((k + 1) * kBatch, nc, nr, nu);
                 ubatch = __shfl(nu, kBatch - 1);
             }
-            const int nbase = (qb == kBatchGroups - 1) ? oth : cur + (qb + 1) * kGroup * 4;
-            const int64_t s0 = q * kGroup;
+            const int nbase = (qb == kRBatchGroups - 1) ? oth : cur + (qb + 1) * kRGroup * 4;
+            const int64_t s0 = q * kRGroup;
 #define ALS_RSTEP(BT, BX, R, J)                                                              \
             {                                                                                \
                 const bool ok = 4 * (s0 + (J)) + g < total;                                  \
@@ -712,11 +878,17 @@ Layout make_layout(const int* waves, int nb_max, int cus) {
     return L;
 }
 
+// Resident waves per CU of both gather forms (the partition is shared, so every wave of either
+// form is resident at once).
 template <int NB>
 int occupancy_waves(int cus, int* waves) {
-    int blocks = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_herm_solve<NB>, kWave, 0);
+    int blocks = 0, blocks_g = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_herm_solve<NB, true>,
+                                                                kWave, 0);
     if (e != hipSuccess) return -1;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_g, k_herm_solve<NB, false>, kWave, 0);
+    if (e != hipSuccess) return -1;
+    if (blocks_g < blocks) blocks = blocks_g;
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxWavesPerCU) blocks = kMaxWavesPerCU;
     const char* env = getenv("ALS_WAVES_PER_CU");
@@ -777,6 +949,7 @@ struct als_ctx {
     hipEvent_t* prof_ev;   // 4 events per profiled half-sweep, or null
     int prof_cap;
     int prof_count;
+    bool global_gather;    // use the 64-bit-load gather for every size (ALS_GATHER=global)
 };
 
 namespace {
@@ -816,10 +989,14 @@ int query_device(int device, int f_max, int* cus, int* waves, int* w_cap) {
     return ALS_OK;
 }
 
+// theta sizes (bytes) served by the buffer-load gather: offsets past the end, plus a padding
+// lane's offset, must stay below 2^32
+constexpr uint64_t kBufferGatherMax = 0x7FFFF000ull;
+
 template <int NB>
 void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
-                  int64_t m, int f, float lambda, const float* theta, float* x, hipStream_t st,
-                  int W) {
+                  int64_t m, int64_t n, int f, float lambda, const float* theta, float* x,
+                  hipStream_t st, int W) {
     int64_t* bounds = (int64_t*)(ctx->ws + ctx->lay.bounds);
     float* slots = (float*)(ctx->ws + ctx->lay.slots);
     auto* nonspd = (unsigned long long*)(ctx->ws + ctx->lay.status);
@@ -829,8 +1006,12 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     hipLaunchKernelGGL(k_plan, dim3((W + 1 + 63) / 64), dim3(64), 0, st, rowptr, m, W,
                        (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds);
     if (ev) (void)hipEventRecord(ev[1], st);
-    hipLaunchKernelGGL(k_herm_solve<NB>, dim3(W), dim3(kWave), 0, st, rowptr, colidx, vals,
-                       theta, m, f, lambda, bounds, x, slots, nonspd);
+    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax)
+        hipLaunchKernelGGL((k_herm_solve<NB, true>), dim3(W), dim3(kWave), 0, st, rowptr, colidx,
+                           vals, theta, m, n, f, lambda, bounds, x, slots, nonspd);
+    else
+        hipLaunchKernelGGL((k_herm_solve<NB, false>), dim3(W), dim3(kWave), 0, st, rowptr,
+                           colidx, vals, theta, m, n, f, lambda, bounds, x, slots, nonspd);
     if (ev) (void)hipEventRecord(ev[2], st);
     if (W > 1)
         hipLaunchKernelGGL(k_reduce_solve<NB>, dim3(W - 1), dim3(kWave), 0, st, rowptr, m, W, f,
@@ -869,6 +1050,10 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
     if (rc != ALS_OK) { delete ctx; return rc; }
     ctx->device = device;
     ctx->f_max = f_max;
+    {
+        const char* g = getenv("ALS_GATHER");
+        ctx->global_gather = g && strcmp(g, "global") == 0;
+    }
     ctx->nb_max = nb_of(f_max);
     ctx->lay = make_layout(ctx->waves, ctx->nb_max, ctx->cus);
     if (workspace_bytes < ctx->lay.total) { delete ctx; return ALS_ERR_WORKSPACE; }
@@ -962,15 +1147,15 @@ int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
     if (!guard.ok) return ALS_ERR_DEVICE;
     hipStream_t st = (hipStream_t)stream;
     switch (nb) {
-        case 1: launch_sweep<1>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 2: launch_sweep<2>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 3: launch_sweep<3>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 4: launch_sweep<4>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 5: launch_sweep<5>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 6: launch_sweep<6>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 7: launch_sweep<7>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 8: launch_sweep<8>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
-        case 9: launch_sweep<9>(ctx, rowptr, colidx, vals, m, f, lambda, theta_in, x_out, st, W); break;
+        case 1: launch_sweep<1>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 2: launch_sweep<2>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 3: launch_sweep<3>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 4: launch_sweep<4>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 5: launch_sweep<5>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 6: launch_sweep<6>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 7: launch_sweep<7>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 8: launch_sweep<8>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
+        case 9: launch_sweep<9>(ctx, rowptr, colidx, vals, m, n, f, lambda, theta_in, x_out, st, W); break;
         default: return ALS_ERR_UNSUPPORTED_F;
     }
     hipError_t e = hipGetLastError();

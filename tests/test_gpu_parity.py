@@ -85,8 +85,9 @@ def _handmade(lengths, n, seed):
 @pytest.mark.parametrize("f", [5, 16, 100, 128])
 def test_edge_row_lengths(ctx, orc, f):
     n = 30_000
-    lengths = [0, 1, 2, f - 1, f, f + 1, 3, 63, 64, 65, 0, 127, 128, 129, 255, 256, 257, 0, 0,
-               511, 1000, 4095, 4096, 4097, 20_000, 1, 0]
+    lengths = [0, 1, 2, f - 1, f, f + 1, 3, 15, 16, 17, 47, 48, 49, 95, 96, 97, 63, 64, 65, 0,
+               127, 128, 129, 143, 144, 145, 255, 256, 257, 0, 0, 511, 1000, 4095, 4096, 4097,
+               20_000, 1, 0]
     lengths = [max(0, k) for k in lengths]
     rowptr, colidx, vals = _handmade(lengths, n, seed=f)
     theta = synthetic_factor(n, f, 91 + f, 0.2)
@@ -94,6 +95,36 @@ def test_edge_row_lengths(ctx, orc, f):
                            f"edge lengths f={f}")
     empty = np.array(lengths) == 0
     assert np.all(xg[empty] == 0.0)
+
+
+@pytest.fixture(scope="module")
+def ctx_global():
+    """A context that gathers with 64-bit global loads at every size (the form used when
+    theta exceeds the buffer-load range)."""
+    import os
+    from paper_1603_03820_amd import als
+    os.environ["ALS_GATHER"] = "global"
+    try:
+        return als.Context(0, 128)
+    finally:
+        del os.environ["ALS_GATHER"]
+
+
+@pytest.mark.parametrize("f", [7, 100, 128])
+def test_global_gather_form(ctx_global, orc, f):
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=777)
+    check_lockstep(ctx_global, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"global gather movie-small f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 778, 1.0 / np.sqrt(f))
+    check_lockstep(ctx_global, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"global gather movie-small f={f} item")
+    lengths = [0, 1, 2, f - 1, f, f + 1, 47, 48, 49, 95, 96, 97, 0, 1000, 4097, 0]
+    rowptr, colidx, vals = _handmade(lengths, 20_000, seed=f + 5)
+    theta = synthetic_factor(20_000, f, 95 + f, 0.2)
+    check_lockstep(ctx_global, orc, rowptr, colidx, vals, len(lengths), 20_000, f, 0.05, theta,
+                   f"global gather edge lengths f={f}")
 
 
 def test_partition_bit_exact(ctx, orc):
