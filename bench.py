@@ -51,7 +51,7 @@ def parse():
 
 
 def split_rows(bounds: np.ndarray, rowptr: np.ndarray) -> int:
-    """Rows cut by a wave boundary (finished by the reduce kernel, not by herm_solve)."""
+    """Rows cut by a chunk boundary (finished by the reduce kernel, not by herm_solve)."""
     m = len(rowptr) - 1
     cut = set()
     for u, k in bounds[1:-1]:
@@ -142,8 +142,8 @@ def main():
     gflops = fl_step / (elapsed / args.steps) / 1e9
 
     # dominant kernel: herm_solve (all Gram flops + the solves of rows it finishes)
-    bu, (W_u, *_r) = als.als_plan(ctx, dp.rowptr, p.m, f)
-    bi, (W_i, *_r) = als.als_plan(ctx, dp.colptr, p.n, f)
+    bu, (C_u, _, _, _, W_u, _) = als.als_plan(ctx, dp.rowptr, p.m, f)
+    bi, (C_i, _, _, _, W_i, _) = als.als_plan(ctx, dp.colptr, p.n, f)
     split_u = split_rows(bu.cpu().numpy(), p.rowptr)
     split_i = split_rows(bi.cpu().numpy(), csc[0])
     herm_fl = [nnz * F_h(f) + ((cnt_u > 0).sum() - split_u) * F_s(f),
@@ -188,7 +188,8 @@ def main():
                "reduce_user": round(float(red_ms[:, 0].mean()), 4),
                "reduce_item": round(float(red_ms[:, 1].mean()), 4),
                "plan": round(float(plan_ms.mean()), 4)},
-        "waves": {"user": W_u, "item": W_i, "split_rows_user": split_u, "split_rows_item": split_i},
+        "waves": {"user": W_u, "item": W_i, "chunks_user": C_u, "chunks_item": C_i,
+                  "split_rows_user": split_u, "split_rows_item": split_i},
         "nonspd_rows": nonspd,
         "train_rmse": float(rmse.item()),
         "roofline": roofline,

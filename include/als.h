@@ -60,7 +60,8 @@ typedef struct als_ctx als_ctx;
 
 /* Bytes of device workspace a context on `device` needs for every f <= f_max.  Returns 0 if
    the device cannot be queried or f_max is outside [1, ALS_F_MAX].  The size depends on the
-   device's compute-unit count and f_max only (not on m, n or nnz). */
+   device's compute-unit count and f_max only (not on m, n or nnz); it is dominated by two
+   partial-accumulator slots per work chunk (about 0.6 GB on a 256-CU MI355X at f_max = 128). */
 size_t als_workspace_bytes(int device, int32_t f_max);
 
 /* Create a context on `device` using the caller's device workspace (at least
@@ -105,16 +106,22 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
 int als_status(als_ctx* ctx, void* stream, int64_t* nonspd_rows);
 
 /*
- * The row-to-wave partition a half-sweep with this f would use (integer work, exposed so it
- * can be checked bit for bit).  Each row u costs c_row + c_nnz n_u units on a cost axis with
- * prefix P(u) = c_nnz rowptr[u] + c_row u, T = P(m).  Boundary b of W waves sits at
- * s_b = floor(T b / W): in row u_b, the largest u with P(u) <= s_b, at entry offset
- * k_b = ceil((s_b - P(u_b) - c_row) / c_nnz) clamped to [0, n_u], rounded to the nearest
- * multiple of q and, if not 0, moved to n_u when fewer than q/2 entries would remain.
- * Wave w takes the entries from (u_w, k_w) up to (u_{w+1}, k_{w+1}); a row cut by a
- * boundary is finished by a second pass that sums the pieces in wave order.
- *   bounds_out : DEVICE int64[2 (W+1)], (u_b, k_b) pairs; capacity in pairs
- *   params_out : HOST int64[4] = {W, c_nnz, c_row, q}
+ * The work partition a half-sweep with this f would use (integer work, exposed so it can be
+ * checked bit for bit).  Each row u costs c_row + c_nnz n_u units on a cost axis with prefix
+ * P(u) = c_nnz rowptr[u] + c_row u, T = P(m).  The axis is cut into C chunks: W large chunks
+ * (W = the device's resident waves for this f) cover T1 = T - T2 and C - W small chunks cover
+ * T2 = floor(T / tail_div).  Boundary b sits at s_b = floor(T1 b / W) for b <= W and at
+ * T1 + floor(T2 (b - W) / (C - W)) for b > W: in row u_b, the largest u with P(u) <= s_b, at
+ * entry offset k_b = ceil((s_b - P(u_b) - c_row) / c_nnz) clamped to [0, n_u], rounded to the
+ * nearest multiple of q and, if not 0, moved to n_u when fewer than q/2 entries would remain.
+ * Chunk c takes the entries from (u_c, k_c) up to (u_{c+1}, k_{c+1}); the waves claim chunks in
+ * order from a counter, so the large chunks go first and the small ones even out the finish.  A
+ * row cut by a boundary is finished by a second pass that sums its pieces in chunk order, so the
+ * result does not depend on which wave ran which chunk.
+ *   bounds_out : DEVICE int64[2 (C+1)], (u_b, k_b) pairs; capacity in pairs (>= C + 1, else
+ *                ALS_ERR_INVALID_ARG after params_out is filled, so a first call with
+ *                capacity 0 learns C)
+ *   params_out : HOST int64[6] = {C, c_nnz, c_row, q, W, tail_div}
  */
 int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t* bounds_out,
              int64_t capacity, int64_t* params_out, void* stream);

@@ -72,7 +72,7 @@ class Oracle:
         lib.oracle_objective.restype = dbl
         lib.oracle_transpose.argtypes = [P, P, P, i64, i64, P, P, P]
         lib.oracle_transpose.restype = ctypes.c_int
-        lib.oracle_partition.argtypes = [P, i64, i64, i64, i64, i64, P]
+        lib.oracle_partition.argtypes = [P, i64, i64, i64, i64, i64, i64, i64, P]
         lib.oracle_partition.restype = ctypes.c_int
         self._lib = lib
 
@@ -127,11 +127,13 @@ class Oracle:
             raise RuntimeError(f"oracle_transpose failed: {rc}")
         return colptr, rowidx, vt
 
-    def partition(self, rowptr, m, W, c_nnz, c_row, q):
-        """int64 [W+1, 2]: (row, entry offset) of each worker boundary."""
-        out = np.empty((W + 1, 2), dtype=np.int64)
+    def partition(self, rowptr, m, W, c_nnz, c_row, q, C=None, tail_div=8):
+        """int64 [C+1, 2]: (row, entry offset) of each chunk boundary; C = W (the default)
+        gives W equal chunks."""
+        C = W if C is None else C
+        out = np.empty((C + 1, 2), dtype=np.int64)
         rc = self._lib.oracle_partition(self._p(np.ascontiguousarray(rowptr, dtype=np.int64)),
-                                        m, W, c_nnz, c_row, q, self._p(out))
+                                        m, W, C, tail_div, c_nnz, c_row, q, self._p(out))
         if rc != 0:
             raise RuntimeError(f"oracle_partition failed: {rc}")
         return out

@@ -246,21 +246,26 @@ int oracle_transpose(const int64_t* rowptr, const int32_t* colidx, const float* 
 /*
  * The work partition of the HIP path, restated from its definition so that the library's
  * integer planning can be checked bit for bit.  Each row u costs c_row + c_nnz * n_u units
- * on a cost axis with prefix P(u) = c_nnz * rowptr[u] + c_row * u (T = P(m)).  Boundary b of
- * W workers sits at s_b = floor(T b / W): in row u_b, the largest u with P(u) <= s_b, at entry
- * offset ceil((s_b - P(u_b) - c_row) / c_nnz) clamped to [0, n_u], rounded to the nearest
- * multiple of q and, if that is not 0, moved to the row end when fewer than q/2 entries would
- * remain.
- * bounds_out[2b] = u_b, bounds_out[2b+1] = that offset; b = 0..W.
+ * on a cost axis with prefix P(u) = c_nnz * rowptr[u] + c_row * u (T = P(m)).  The axis is cut
+ * into C chunks: W equal "large" chunks cover T1 = T - T2 and C - W equal "small" chunks cover
+ * the tail T2 = floor(T / tail_div) (T2 = 0 when C = W).  Boundary b sits at
+ *     s_b = floor(T1 b / W)                          for b <= W,
+ *     s_b = T1 + floor(T2 (b - W) / (C - W))         for b >= W,
+ * in row u_b, the largest u with P(u) <= s_b, at entry offset ceil((s_b - P(u_b) - c_row) /
+ * c_nnz) clamped to [0, n_u], rounded to the nearest multiple of q and, if that is not 0, moved
+ * to the row end when fewer than q/2 entries would remain.
+ * bounds_out[2b] = u_b, bounds_out[2b+1] = that offset; b = 0..C.
  */
-int oracle_partition(const int64_t* rowptr, int64_t m, int64_t W, int64_t c_nnz, int64_t c_row,
-                     int64_t q, int64_t* bounds_out) {
-    if (!rowptr || m < 0 || W < 1 || c_nnz < 1 || c_row < 1 || q < 2 || (q & 1) || !bounds_out)
+int oracle_partition(const int64_t* rowptr, int64_t m, int64_t W, int64_t C, int64_t tail_div,
+                     int64_t c_nnz, int64_t c_row, int64_t q, int64_t* bounds_out) {
+    if (!rowptr || m < 0 || W < 1 || C < W || tail_div < 1 || c_nnz < 1 || c_row < 1 || q < 2 ||
+        (q & 1) || !bounds_out)
         return ORACLE_ERR_ARG;
     const __int128 T = (__int128)c_nnz * rowptr[m] + (__int128)c_row * m;
+    const __int128 T2 = C > W ? T / tail_div : 0, T1 = T - T2;
     int64_t u = 0; /* s_b grows with b, so u_b does too: scan on from the previous one */
-    for (int64_t b = 0; b <= W; ++b) {
-        const __int128 s = T * b / W;
+    for (int64_t b = 0; b <= C; ++b) {
+        const __int128 s = b <= W ? T1 * b / W : T1 + T2 * (b - W) / (C - W);
         while (u < m && (__int128)c_nnz * rowptr[u + 1] + (__int128)c_row * (u + 1) <= s) ++u;
         int64_t kk = 0;
         if (u < m) {

@@ -161,17 +161,17 @@ def als_status(ctx: Context, stream=None) -> int:
 
 
 def als_plan(ctx: Context, rowptr, m: int, f: int, stream=None):
-    """(bounds int64 [W+1, 2] device tensor, (W, c_nnz, c_row, q))."""
-    params = (ctypes.c_int64 * 4)()
-    # first call with zero capacity to learn W
+    """(bounds int64 [C+1, 2] device tensor, (C, c_nnz, c_row, q, W, tail_div))."""
+    params = (ctypes.c_int64 * 6)()
+    # first call with zero capacity to learn C
     rc = _lib.als_plan(ctx.handle, _dev(rowptr, torch.int64, "rowptr", m + 1), m, f,
                        ctypes.c_void_p(rowptr.data_ptr()), 0, params, _stream(ctx.device, stream))
     if rc not in (ALS_OK, -1):
         _check("als_plan", rc, ctx.handle)
-    W = int(params[0])
-    bounds = torch.empty((W + 1, 2), dtype=torch.int64, device=ctx.device)
+    C = int(params[0])
+    bounds = torch.empty((C + 1, 2), dtype=torch.int64, device=ctx.device)
     rc = _lib.als_plan(ctx.handle, _dev(rowptr, torch.int64, "rowptr", m + 1), m, f,
-                       _dev(bounds, torch.int64, "bounds"), W + 1, params,
+                       _dev(bounds, torch.int64, "bounds"), C + 1, params,
                        _stream(ctx.device, stream))
     _check("als_plan", rc, ctx.handle)
     return bounds, tuple(int(v) for v in params)

@@ -43,6 +43,9 @@ constexpr int kWave = 64;
 constexpr int kMaxNB = ALS_F_MAX / 16 + 1;      // 9 column blocks of 16 cover f + 1 <= 129
 constexpr int kSnap = 256;                      // partition cut grid (entries)
 constexpr int kCostPerEntry = 16;               // c_nnz
+constexpr int kTailDiv = 8;                     // the small chunks cover floor(T / 8) of the cost
+constexpr int kSmallPerWave = 4;                // small chunks per wave
+constexpr int chunks_of(int waves) { return waves * (1 + kSmallPerWave); }
 constexpr int kMaxWavesPerCU = 32;
 constexpr int kRmseWavesPerCU = 24;                // RMSE: 6 waves per SIMD, latency hiding
 
@@ -102,14 +105,25 @@ __device__ __forceinline__ float row_sum16(float v) {
 
 // ------------------------------------------------------------------------------- plan ----
 
-// Cost prefix P(u) = c_nnz rowptr[u] + c_row u; boundary b at s_b = floor(T b / W).
-__global__ void k_plan(const int64_t* __restrict__ rowptr, int64_t m, int W, int64_t c_nnz,
-                       int64_t c_row, int64_t q, int64_t* __restrict__ bounds) {
+// Cost prefix P(u) = c_nnz rowptr[u] + c_row u, T = P(m).  C chunks: W large ones cover
+// T1 = T - T2 and C - W small ones the tail T2 = floor(T / kTailDiv) (T2 = 0 when C = W);
+// boundary b sits at s_b = floor(T1 b / W) for b <= W, T1 + floor(T2 (b - W) / (C - W)) beyond.
+// Thread 0 also resets the chunk counter the persistent waves claim chunks from.
+__global__ void k_plan(const int64_t* __restrict__ rowptr, int64_t m, int W, int C, int64_t c_nnz,
+                       int64_t c_row, int64_t q, int64_t* __restrict__ bounds,
+                       unsigned* __restrict__ chunk_ctr) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b > W) return;
+    if (b == 0 && chunk_ctr) *chunk_ctr = 0u;
+    if (b > C) return;
     const int64_t T = c_nnz * rowptr[m] + c_row * m;
-    const int64_t Q = T / W, R = T % W;
-    const int64_t s = Q * b + (R * b) / W;   // == floor(T b / W) without 128-bit products
+    const int64_t T2 = C > W ? T / kTailDiv : 0, T1 = T - T2;
+    int64_t s;   // floor(X b / D) as Q b + floor(R b / D), without 128-bit products
+    if (b <= W) {
+        s = T1 / W * b + (T1 % W) * b / W;
+    } else {
+        const int64_t D = C - W, e = b - W;
+        s = T1 + T2 / D * e + (T2 % D) * e / D;
+    }
     int64_t lo = 0, hi = m;                  // largest u in [0, m] with P(u) <= s
     while (lo < hi) {
         const int64_t mid = (lo + hi + 1) >> 1;
@@ -575,33 +589,41 @@ __device__ __forceinline__ void write_zero_row(float* __restrict__ xrow, int f, 
     for (int j = lane; j < f; j += kWave) xrow[j] = 0.f;
 }
 
+// A partial-accumulator slot: tile t of lane l at f4 index 64 t + l (16 contiguous bytes per
+// lane, 1 KiB per tile).
 template <int NB>
 __device__ __forceinline__ void store_slot(const f4 (&acc)[ntiles(NB)], float* __restrict__ slot,
                                            int lane) {
+    f4* s = reinterpret_cast<f4*>(slot);
 #pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) slot[(t * 4 + r) * kWave + lane] = acc[t][r];
+    for (int t = 0; t < ntiles(NB); ++t) s[t * kWave + lane] = acc[t];
 }
 
+// acc += slot.  All loads are issued before the first add (a dependent load-add chain would
+// leave one load in flight at a time).
 template <int NB>
 __device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], const float* __restrict__ slot,
                                          int lane) {
+    const f4* s = reinterpret_cast<const f4*>(slot);
+    f4 v[ntiles(NB)];
 #pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t)
+    for (int t = 0; t < ntiles(NB); ++t) v[t] = s[t * kWave + lane];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[t][r] += slot[(t * 4 + r) * kWave + lane];
+    for (int t = 0; t < ntiles(NB); ++t) acc[t] += v[t];
 }
 
 // ------------------------------------------------------------------------ kernels --------
 
-// Wave w: entries from bounds[w] to bounds[w+1].  Whole rows are solved here; the piece of a
-// row cut at the start of the share goes to slot 2w, the piece cut at its end to slot 2w+1.
-// Rows are software-pipelined: the next piece's index batches load while this piece's Gram
-// runs, and its first theta gathers are in flight while this piece is solved.
+// Persistent waves claim chunks in order from a counter; chunk c covers the entries from
+// bounds[c] to bounds[c+1].  Whole rows are solved here; the piece of a row cut at the start of
+// the chunk goes to slot 2c, the piece cut at its end to slot 2c+1, so what is stored where does
+// not depend on which wave ran the chunk.  Rows are software-pipelined: the next piece's index
+// batches load while this piece's Gram runs, and its first theta gathers are in flight while
+// this piece is solved.
 struct Piece {
     int64_t u, beg, end;   // row, entry range [beg, end)
-    bool whole;            // the share holds the whole row
+    bool whole;            // the chunk holds the whole row
 };
 
 template <int NB, bool BUF>
@@ -609,106 +631,190 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 7 ?
 void k_herm_solve(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int64_t n,
-    int f, float lambda, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
-    float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
+    int f, float lambda, int C, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
+    float* __restrict__ slots, unsigned long long* __restrict__ nonspd,
+    unsigned* __restrict__ chunk_ctr) {
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
     __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x;
-    const int w = blockIdx.x;
-    const int64_t u0 = bounds[2 * w], k0 = bounds[2 * w + 1];
-    const int64_t u1 = bounds[2 * w + 2], k1 = bounds[2 * w + 3];
-    // the first piece with entries at or after row u; empty rows on the way get x_u = 0
-    auto next_piece = [&](int64_t u, Piece& p) -> bool {
-        for (; u <= u1 && u < m; ++u) {
-            const int64_t rs = rowptr[u], nu = rowptr[u + 1] - rs;
-            const int64_t ka = (u == u0) ? k0 : 0;
-            int64_t kb = nu;
-            if (u == u1) {
-                if (k1 == 0) return false;
-                kb = k1;
-            }
-            if (nu == 0) {
-                write_zero_row<NB>(x_out + (size_t)u * f, f, lane);
-                continue;
-            }
-            if (ka >= kb) continue;
-            p = Piece{u, rs + ka, rs + kb, ka == 0 && kb == nu};
-            return true;
-        }
-        return false;
-    };
-    Piece cur;
-    if (!next_piece(u0, cur)) return;
     const Gather<NB, BUF> gat(theta, n, f, lane & 15);
-    RowIndex ix;
-    Inflight<NB> in;
-    gram_prefetch(gat, colidx, vals, cur.beg, cur.end, lane, ix);
-    gram_stage<NB>(gat, ix, ring, lane, in);
     for (;;) {
-        Piece nxt;
-        const bool more = next_piece(cur.u + 1, nxt);
-        if (more) gram_prefetch(gat, colidx, vals, nxt.beg, nxt.end, lane, ix);
-        f4 acc[ntiles(NB)];
+        int claim = 0;
+        if (lane == 0) claim = (int)atomicAdd(chunk_ctr, 1u);
+        const int c = __builtin_amdgcn_readfirstlane(claim);
+        if (c >= C) break;
+        const int64_t u0 = bounds[2 * c], k0 = bounds[2 * c + 1];
+        const int64_t u1 = bounds[2 * c + 2], k1 = bounds[2 * c + 3];
+        // the first piece with entries at or after row u; empty rows on the way get x_u = 0
+        auto next_piece = [&](int64_t u, Piece& p) -> bool {
+            for (; u <= u1 && u < m; ++u) {
+                const int64_t rs = rowptr[u], nu = rowptr[u + 1] - rs;
+                const int64_t ka = (u == u0) ? k0 : 0;
+                int64_t kb = nu;
+                if (u == u1) {
+                    if (k1 == 0) return false;
+                    kb = k1;
+                }
+                if (nu == 0) {
+                    write_zero_row<NB>(x_out + (size_t)u * f, f, lane);
+                    continue;
+                }
+                if (ka >= kb) continue;
+                p = Piece{u, rs + ka, rs + kb, ka == 0 && kb == nu};
+                return true;
+            }
+            return false;
+        };
+        Piece cur;
+        if (!next_piece(u0, cur)) continue;
+        RowIndex ix;
+        Inflight<NB> in;
+        gram_prefetch(gat, colidx, vals, cur.beg, cur.end, lane, ix);
+        gram_stage<NB>(gat, ix, ring, lane, in);
+        for (;;) {
+            Piece nxt;
+            const bool more = next_piece(cur.u + 1, nxt);
+            if (more) gram_prefetch(gat, colidx, vals, nxt.beg, nxt.end, lane, ix);
+            f4 acc[ntiles(NB)];
 #pragma unroll
-        for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-        gram_loop<NB>(gat, colidx, vals, cur.beg, cur.end, acc, ring, lane, in);
-        if (more) gram_stage<NB>(gat, ix, ring, lane, in);
-        // the solve is a latency-bound chain; raised priority lets it win issue slots over the
-        // other wave's independent Gram MFMAs, which then fill the solve's gaps
-        __builtin_amdgcn_s_setprio(2);
-        if (cur.whole) {
-            const int64_t nu = cur.end - cur.beg;
-            const float lam_n = (float)((double)lambda * (double)nu);
-            if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)cur.u * f, lane) && lane == 0)
-                atomicAdd(nonspd, 1ull);
-        } else {
-            const int which = (cur.u == u0) ? 0 : 1;
-            store_slot<NB>(acc, slots + (size_t)(2 * w + which) * slot_floats(NB), lane);
+            for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+            gram_loop<NB>(gat, colidx, vals, cur.beg, cur.end, acc, ring, lane, in);
+            if (more) gram_stage<NB>(gat, ix, ring, lane, in);
+            // the solve is a latency-bound chain; raised priority lets it win issue slots over
+            // the other wave's independent Gram MFMAs, which then fill the solve's gaps
+            __builtin_amdgcn_s_setprio(2);
+            if (cur.whole) {
+                const int64_t nu = cur.end - cur.beg;
+                const float lam_n = (float)((double)lambda * (double)nu);
+                if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)cur.u * f, lane) &&
+                    lane == 0)
+                    atomicAdd(nonspd, 1ull);
+            } else {
+                const int which = (cur.u == u0) ? 0 : 1;
+                store_slot<NB>(acc, slots + (size_t)(2 * c + which) * slot_floats(NB), lane);
+            }
+            __builtin_amdgcn_s_setprio(0);
+            if (!more) break;
+            cur = nxt;
         }
-        __builtin_amdgcn_s_setprio(0);
-        if (!more) break;
-        cur = nxt;
     }
 }
 
-// One wave per internal boundary b (1..W-1); the first boundary that cuts a row sums that
-// row's pieces -- wave b-1's, then b, b+1, ... -- and solves it.
+// Rows cut by chunk boundaries.  Row u's pieces are: the first, held by chunk b_first - 1 (as
+// that chunk's first piece if it started in row u, else as its last), then the piece starting at
+// each boundary b_first..b_last that cuts u, in slot 2b (empty, and unwritten, when several
+// boundaries snapped to one cut point).  The boundaries cutting one row are consecutive, so both
+// ends are found by binary search over the sorted bounds.  A row with more than kPieceGroup
+// boundary pieces is summed in two passes: every kPieceGroup-th boundary leads a group and sums
+// the group's pieces, in chunk order, into its own slot; then the row's first boundary adds the
+// first piece and the group sums, in order, and solves.  The order is fixed, so the result does
+// not depend on timing.
+constexpr int kPieceGroup = 16;
+
+__device__ __forceinline__ bool cuts_row(const int64_t* __restrict__ rowptr, int64_t m,
+                                         const int64_t* __restrict__ bounds, int b) {
+    const int64_t u = bounds[2 * b], k = bounds[2 * b + 1];
+    return u < m && k > 0 && k < rowptr[u + 1] - rowptr[u];
+}
+
+// First and last boundary in [1, C-1] that cut row u, given that boundary b does.
+__device__ __forceinline__ void cut_range(const int64_t* __restrict__ rowptr, int64_t m,
+                                          const int64_t* __restrict__ bounds, int C, int b,
+                                          int64_t u, int& b_first, int& b_last) {
+    // boundaries with row u and an offset strictly inside it form one run around b (bounds are
+    // sorted by (row, offset): one of row u at offset 0 precedes the run, one at n_u follows it)
+    int lo = 1, hi = b;   // first boundary >= 1 in the run
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (bounds[2 * mid] < u || !cuts_row(rowptr, m, bounds, mid)) lo = mid + 1; else hi = mid;
+    }
+    b_first = lo;
+    lo = b; hi = C - 1;   // last boundary <= C-1 in the run
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (bounds[2 * mid] == u && cuts_row(rowptr, m, bounds, mid)) lo = mid; else hi = mid - 1;
+    }
+    b_last = lo;
+}
+
+// Add the non-empty boundary pieces of row u for boundaries bb in [from, to] into acc.
 template <int NB>
-__global__ __launch_bounds__(kWave) void k_reduce_solve(
-    const int64_t* __restrict__ rowptr, int64_t m, int W, int f, float lambda,
-    const int64_t* __restrict__ bounds, float* __restrict__ x_out,
-    const float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
-    __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
+__device__ __forceinline__ void add_pieces(f4 (&acc)[ntiles(NB)], const int64_t* __restrict__ bounds,
+                                           const float* __restrict__ slots, int from, int to,
+                                           int b_last, int64_t nu, int lane) {
+    for (int bb = from; bb <= to; ++bb) {
+        // the piece of chunk bb runs to the next boundary in the row, or to the row's end
+        const int64_t piece_end = bb < b_last ? bounds[2 * (bb + 1) + 1] : nu;
+        if (bounds[2 * bb + 1] < piece_end)
+            add_slot<NB>(acc, slots + (size_t)(2 * bb) * slot_floats(NB), lane);
+    }
+}
+
+// Pass 1: one wave per internal boundary (the loop also serves smaller grids); group leaders of
+// long cut rows sum their group.
+template <int NB>
+__global__ __launch_bounds__(kWave) void k_reduce_groups(
+    const int64_t* __restrict__ rowptr, int64_t m, int C, const int64_t* __restrict__ bounds,
+    float* __restrict__ slots) {
     const int lane = threadIdx.x;
-    const int b = blockIdx.x + 1;
-    if (b >= W) return;
-    auto cuts = [&](int bb) -> bool {   // boundary bb lies strictly inside its row
-        const int64_t u = bounds[2 * bb], k = bounds[2 * bb + 1];
-        return u < m && k > 0 && k < rowptr[u + 1] - rowptr[u];
-    };
-    if (!cuts(b)) return;
+    for (int b = blockIdx.x + 1; b < C; b += gridDim.x) {
+        if (!cuts_row(rowptr, m, bounds, b)) continue;
+        const int64_t u = bounds[2 * b];
+        int b_first, b_last;
+        cut_range(rowptr, m, bounds, C, b, u, b_first, b_last);
+        if (b_last - b_first + 1 <= kPieceGroup || (b - b_first) % kPieceGroup != 0) continue;
+        f4 acc[ntiles(NB)];
+#pragma unroll
+        for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+        const int to = b + kPieceGroup - 1 < b_last ? b + kPieceGroup - 1 : b_last;
+        add_pieces<NB>(acc, bounds, slots, b, to, b_last, rowptr[u + 1] - rowptr[u], lane);
+        store_slot<NB>(acc, slots + (size_t)(2 * b) * slot_floats(NB), lane);
+    }
+}
+
+// Pass 2: one wave per internal boundary (the loop also serves smaller grids); the first
+// boundary that cuts a row sums its pieces (or its group sums) and solves it.
+template <int NB>
+__device__ __forceinline__ void reduce_row(const int64_t* __restrict__ rowptr, int64_t m, int C,
+                                           int f, float lambda, const int64_t* __restrict__ bounds,
+                                           float* __restrict__ x_out,
+                                           const float* __restrict__ slots,
+                                           unsigned long long* __restrict__ nonspd,
+                                           SolveLds<NB>& lds, int b, int lane) {
+    if (!cuts_row(rowptr, m, bounds, b)) return;
     const int64_t u = bounds[2 * b];
-    if (b > 1 && cuts(b - 1) && bounds[2 * (b - 1)] == u) return;   // not the first cut
+    if (b > 1 && cuts_row(rowptr, m, bounds, b - 1) && bounds[2 * (b - 1)] == u)
+        return;   // not the first cut
+    int b_first, b_last;
+    cut_range(rowptr, m, bounds, C, b, u, b_first, b_last);
     f4 acc[ntiles(NB)];
 #pragma unroll
     for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-    // wave b-1 holds the row's first piece: as its first piece if it started in row u
+    // chunk b-1 holds the row's first piece: as its first piece if it started in row u
     // (then at entry 0), else as its last piece
     const int first_slot = (bounds[2 * (b - 1)] == u) ? 2 * (b - 1) : 2 * (b - 1) + 1;
     add_slot<NB>(acc, slots + (size_t)first_slot * slot_floats(NB), lane);
     const int64_t nu = rowptr[u + 1] - rowptr[u];
-    for (int bb = b;; ++bb) {   // waves b, b+1, ... start inside row u: their first piece
-        const bool more = bb + 1 < W && cuts(bb + 1) && bounds[2 * (bb + 1)] == u;
-        // several boundaries can snap to one cut point; the waves between them hold an empty
-        // piece of row u and wrote no slot
-        const int64_t piece_end = more ? bounds[2 * (bb + 1) + 1] : nu;
-        if (bounds[2 * bb + 1] < piece_end)
-            add_slot<NB>(acc, slots + (size_t)(2 * bb) * slot_floats(NB), lane);
-        if (!more) break;
+    if (b_last - b_first + 1 <= kPieceGroup) {
+        add_pieces<NB>(acc, bounds, slots, b, b_last, b_last, nu, lane);
+    } else {
+        for (int g = b; g <= b_last; g += kPieceGroup)
+            add_slot<NB>(acc, slots + (size_t)(2 * g) * slot_floats(NB), lane);
     }
     const float lam_n = (float)((double)lambda * (double)nu);
     if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane) && lane == 0)
         atomicAdd(nonspd, 1ull);
+}
+
+template <int NB>
+__global__ __launch_bounds__(kWave) void k_reduce_solve(
+    const int64_t* __restrict__ rowptr, int64_t m, int C, int f, float lambda,
+    const int64_t* __restrict__ bounds, float* __restrict__ x_out,
+    const float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
+    __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
+    for (int b = blockIdx.x + 1; b < C; b += gridDim.x)
+        reduce_row<NB>(rowptr, m, C, f, lambda, bounds, x_out, slots, nonspd, lds, b,
+                       threadIdx.x);
 }
 
 // RMSE pipeline shape: groups of three steps with three buffers, batches of four groups.
@@ -859,19 +965,21 @@ struct Layout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// waves[nb] = W for f in (16 (nb-1), 16 nb]; the slot region holds 2 W partial accumulators
+// waves[nb] = W for f in (16 (nb-1), 16 nb]; the slot region holds 2 C partial accumulators,
+// C = chunks_of(W)
 Layout make_layout(const int* waves, int nb_max, int cus) {
-    int w_cap = 1;
+    int c_cap = 1;
     size_t slot_bytes = 0;
     for (int nb = 1; nb <= nb_max; ++nb) {
-        if (waves[nb] > w_cap) w_cap = waves[nb];
-        const size_t sb = sizeof(float) * (size_t)slot_floats(nb) * 2 * (size_t)waves[nb];
+        const int C = chunks_of(waves[nb]);
+        if (C > c_cap) c_cap = C;
+        const size_t sb = sizeof(float) * (size_t)slot_floats(nb) * 2 * (size_t)C;
         if (sb > slot_bytes) slot_bytes = sb;
     }
     Layout L;
     size_t off = 0;
-    L.status = off; off = align256(off + 256);
-    L.bounds = off; off = align256(off + sizeof(int64_t) * 2 * (size_t)(w_cap + 1));
+    L.status = off; off = align256(off + 256);   // non-SPD counter at 0, chunk counter at 64
+    L.bounds = off; off = align256(off + sizeof(int64_t) * 2 * (size_t)(c_cap + 1));
     L.rmse = off;   off = align256(off + sizeof(double) * (size_t)cus * kRmseWavesPerCU);
     L.slots = off;  off = align256(off + slot_bytes);
     L.total = off;
@@ -1000,22 +1108,29 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     int64_t* bounds = (int64_t*)(ctx->ws + ctx->lay.bounds);
     float* slots = (float*)(ctx->ws + ctx->lay.slots);
     auto* nonspd = (unsigned long long*)(ctx->ws + ctx->lay.status);
+    auto* chunk_ctr = (unsigned*)(ctx->ws + ctx->lay.status + 64);
+    const int C = chunks_of(W);
     hipEvent_t* ev = nullptr;
     if (ctx->prof_ev && ctx->prof_count < ctx->prof_cap) ev = ctx->prof_ev + 4 * ctx->prof_count++;
     if (ev) (void)hipEventRecord(ev[0], st);
-    hipLaunchKernelGGL(k_plan, dim3((W + 1 + 63) / 64), dim3(64), 0, st, rowptr, m, W,
-                       (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds);
+    hipLaunchKernelGGL(k_plan, dim3((C + 1 + 63) / 64), dim3(64), 0, st, rowptr, m, W, C,
+                       (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds, chunk_ctr);
     if (ev) (void)hipEventRecord(ev[1], st);
     if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax)
         hipLaunchKernelGGL((k_herm_solve<NB, true>), dim3(W), dim3(kWave), 0, st, rowptr, colidx,
-                           vals, theta, m, n, f, lambda, bounds, x, slots, nonspd);
+                           vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd, chunk_ctr);
     else
         hipLaunchKernelGGL((k_herm_solve<NB, false>), dim3(W), dim3(kWave), 0, st, rowptr,
-                           colidx, vals, theta, m, n, f, lambda, bounds, x, slots, nonspd);
+                           colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
+                           chunk_ctr);
     if (ev) (void)hipEventRecord(ev[2], st);
-    if (W > 1)
-        hipLaunchKernelGGL(k_reduce_solve<NB>, dim3(W - 1), dim3(kWave), 0, st, rowptr, m, W, f,
+    if (C > 1) {
+        // one wave per boundary: the rows' solves run side by side
+        hipLaunchKernelGGL(k_reduce_groups<NB>, dim3(C - 1), dim3(kWave), 0, st, rowptr, m, C,
+                           bounds, slots);
+        hipLaunchKernelGGL(k_reduce_solve<NB>, dim3(C - 1), dim3(kWave), 0, st, rowptr, m, C, f,
                            lambda, bounds, x, slots, nonspd);
+    }
     if (ev) (void)hipEventRecord(ev[3], st);
 }
 
@@ -1219,15 +1334,19 @@ int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t*
     if (f < 1 || f > ctx->f_max) return ALS_ERR_UNSUPPORTED_F;
     if (!aligned(rowptr, 8) || !aligned(bounds_out, 8)) return ALS_ERR_ALIGN;
     const int W = ctx->waves[nb_of(f)];
-    params_out[0] = W;
+    const int C = chunks_of(W);
+    params_out[0] = C;
     params_out[1] = kCostPerEntry;
     params_out[2] = row_cost(f);
     params_out[3] = kSnap;
-    if (capacity < W + 1) return ALS_ERR_INVALID_ARG;
+    params_out[4] = W;
+    params_out[5] = kTailDiv;
+    if (capacity < C + 1) return ALS_ERR_INVALID_ARG;
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
-    hipLaunchKernelGGL(k_plan, dim3((W + 1 + 63) / 64), dim3(64), 0, (hipStream_t)stream, rowptr,
-                       m, W, (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds_out);
+    hipLaunchKernelGGL(k_plan, dim3((C + 1 + 63) / 64), dim3(64), 0, (hipStream_t)stream, rowptr,
+                       m, W, C, (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds_out,
+                       nullptr);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
 }

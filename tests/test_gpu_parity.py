@@ -127,6 +127,27 @@ def test_global_gather_form(ctx_global, orc, f):
                    f"global gather edge lengths f={f}")
 
 
+@pytest.mark.parametrize("f", [16, 100])
+def test_long_row_in_small_chunks(ctx, orc, f):
+    """A very long row at the end of the cost axis is cut by many small chunks; its pieces are
+    summed in groups before the solve."""
+    from paper_1603_03820_amd import als
+    n = 250_000
+    lengths = [40, 0, 3, 700] * 50 + [200_000, 5, 0, 90_000, 17]
+    rowptr, colidx, vals = _handmade(lengths, n, seed=31 + f)
+    m = len(lengths)
+    bounds, (C, _, _, _, W, _) = als.als_plan(ctx, to_dev(rowptr, ctx.device), m, f)
+    b = bounds.cpu().numpy()
+    nus = np.diff(rowptr)
+    cut = [(u, k) for u, k in b[1:C] if u < m and 0 < k < nus[u]]
+    runs = np.bincount([u for u, _ in cut], minlength=m)
+    log(f"long-row plan: C={C} W={W} longest run of cuts {runs.max()}")
+    assert runs.max() > 16, "the grouped reduce must be exercised"
+    theta = synthetic_factor(n, f, 300 + f, 0.1)
+    check_lockstep(ctx, orc, rowptr, colidx, vals, m, n, f, 0.05, theta,
+                   f"long rows in small chunks f={f}")
+
+
 def test_partition_bit_exact(ctx, orc):
     from paper_1603_03820_amd import als
     cases = []
@@ -140,9 +161,11 @@ def test_partition_bit_exact(ctx, orc):
     for rowptr, f in cases:
         m = len(rowptr) - 1
         log(f"plan m={m} nnz={int(rowptr[-1])} f={f}")
-        bounds, (W, c_nnz, c_row, q) = als.als_plan(ctx, to_dev(rowptr, ctx.device), m, f)
+        bounds, (C, c_nnz, c_row, q, W, tail_div) = als.als_plan(ctx, to_dev(rowptr, ctx.device),
+                                                                 m, f)
         torch.cuda.synchronize()
-        ref = orc.partition(rowptr, m, W, c_nnz, c_row, q)
+        assert C > W >= 1
+        ref = orc.partition(rowptr, m, W, c_nnz, c_row, q, C=C, tail_div=tail_div)
         assert np.array_equal(bounds.cpu().numpy(), ref)
 
 

@@ -51,16 +51,19 @@ def _cases():
     return cases
 
 
+@pytest.mark.parametrize("tiers", [1, 5])
 @pytest.mark.parametrize("case", range(len(_cases())))
-def test_partition_properties(oracle_lib, case):
+def test_partition_properties(oracle_lib, case, tiers):
     rowptr, W, c_nnz, c_row, q = _cases()[case]
+    C = tiers * W   # tiers = 5: W large chunks, then 4 W small ones over the last T / 8
     m = len(rowptr) - 1
-    bounds = oracle_lib.partition(rowptr, m, W, c_nnz, c_row, q)
-    assert tuple(bounds[0]) == (0, 0) and tuple(bounds[W]) == (m, 0)
-    for b in range(W):
+    bounds = oracle_lib.partition(rowptr, m, W, c_nnz, c_row, q, C=C, tail_div=8)
+    assert bounds.shape == (C + 1, 2)
+    assert tuple(bounds[0]) == (0, 0) and tuple(bounds[C]) == (m, 0)
+    for b in range(C):
         assert tuple(bounds[b]) <= tuple(bounds[b + 1]), "boundaries must be monotone"
     nus = np.diff(rowptr)
-    for u, kk in bounds[1:W]:
+    for u, kk in bounds[1:C]:
         if u < m:
             assert 0 <= kk <= nus[u]
             assert kk == nus[u] or kk % q == 0
@@ -74,14 +77,33 @@ def test_partition_properties(oracle_lib, case):
     assert np.all(seen == 1)
     assert np.all(pieces_per_row >= 1)
     assert np.all(pieces_per_row[nus == 0] == 1), "an empty row must be written exactly once"
-    # balance: each worker's share of the cost axis is within one row cost plus one snap of T/W
+    # balance: each chunk's share of the cost axis is within one row cost plus one snap of its
+    # tier's ideal size (T1 / W for the large chunks, T2 / (C - W) for the small ones)
     T = c_nnz * int(rowptr[-1]) + c_row * m
-    cost = np.zeros(W)
+    T2 = T // 8 if C > W else 0
+    T1 = T - T2
+    ideal = np.array([T1 / W] * W + ([T2 / (C - W)] * (C - W) if C > W else []))
+    cost = np.zeros(C)
     for w, u, ka, kb in portions(bounds, rowptr):
         cost[w] += c_nnz * (kb - ka) + (c_row if ka == 0 else 0)
     # each realised cut lies within c_row + c_nnz (q/2 + 1) of its ideal point s_b
     slack = 2 * (c_row + c_nnz * (q // 2 + 1))
-    assert np.all(np.abs(cost - T / W) <= slack)
+    assert np.all(np.abs(cost - ideal) <= slack)
+
+
+def test_single_tier_matches_equal_split(oracle_lib):
+    # C = W: boundaries at floor(T b / W), the equal split
+    rowptr = np.cumsum(np.r_[0, np.arange(1, 300) % 23]).astype(np.int64)
+    a = oracle_lib.partition(rowptr, 299, 41, 16, 900, 64)
+    b = oracle_lib.partition(rowptr, 299, 41, 16, 900, 64, C=41, tail_div=3)
+    assert np.array_equal(a, b)
+    # the large tier of a two-tier plan cuts T - floor(T/8) into W equal parts: where T / 8 is
+    # a whole number of rows at the end, the first W boundaries equal an equal split of the rest
+    rp = np.arange(0, 8 * 10 * 4 + 1, 4, dtype=np.int64)          # 80 rows of 4 entries
+    two = oracle_lib.partition(rp, 80, 5, 16, 64, 2, C=15, tail_div=8)
+    one = oracle_lib.partition(rp[:71], 70, 5, 16, 64, 2)          # first 70 rows = 7/8 of T
+    assert np.array_equal(two[:6], one)
+    assert tuple(two[15]) == (80, 0)
 
 
 def test_partition_is_pure_integer_and_deterministic(oracle_lib):
@@ -136,15 +158,82 @@ def writer_pieces(bounds, rowptr):
     return stored
 
 
+@pytest.mark.parametrize("tiers", [1, 5])
 @pytest.mark.parametrize("W", [3, 17, 200, 2000])
-def test_reducer_reads_exactly_the_stored_pieces(oracle_lib, W):
+def test_reducer_reads_exactly_the_stored_pieces(oracle_lib, W, tiers):
     # few entries per wave: many boundaries snap onto the same cut point
     rp = np.concatenate([[0], np.cumsum([3, 0, 5000, 1, 0, 300, 12000, 7, 900, 0, 4100])])
     rp = rp.astype(np.int64)
-    bounds = oracle_lib.partition(rp, len(rp) - 1, W, 16, 16 * 60, 256)
+    bounds = oracle_lib.partition(rp, len(rp) - 1, W, 16, 16 * 60, 256, C=tiers * W)
     stored = writer_pieces(bounds, rp)
     read = reducer_pieces(bounds, rp)
     read_set = {(w, s): u for u, ps in read.items() for (w, s) in ps}
     assert read_set == stored
     for u, ps in read.items():
         assert [w for w, _ in ps] == sorted(w for w, _ in ps), "pieces summed in wave order"
+
+
+def grouped_reduce(bounds, rowptr, G):
+    """The two-pass reduce's view (groups of G boundary pieces for rows with more than G):
+    returns (pass1, pass2), pass1: leader b -> (slots read in order, slot written),
+    pass2: row -> slots read in order.  Slots are (chunk, 0|1) like writer_pieces."""
+    m, C = len(rowptr) - 1, len(bounds) - 1
+
+    def cuts(b):
+        u, k = bounds[b]
+        return u < m and 0 < k < rowptr[u + 1] - rowptr[u]
+
+    runs = {}   # row -> consecutive boundaries cutting it
+    for b in range(1, C):
+        if cuts(b):
+            runs.setdefault(int(bounds[b][0]), []).append(b)
+    pass1, pass2 = {}, {}
+    for u, bs in runs.items():
+        assert bs == list(range(bs[0], bs[-1] + 1)), "cuts of one row are consecutive"
+        nu = int(rowptr[u + 1] - rowptr[u])
+        b_first, b_last = bs[0], bs[-1]
+
+        def piece_slots(lo, hi):
+            out = []
+            for bb in range(lo, hi + 1):
+                end = int(bounds[bb + 1][1]) if bb < b_last else nu
+                if bounds[bb][1] < end:
+                    out.append((bb, 0))
+            return out
+
+        first = (b_first - 1, 0 if bounds[b_first - 1][0] == u else 1)
+        if len(bs) <= G:
+            pass2[u] = [first] + piece_slots(b_first, b_last)
+        else:
+            reads = [first]
+            for g in range(b_first, b_last + 1, G):
+                pass1[g] = (piece_slots(g, min(g + G - 1, b_last)), (g, 0))
+                reads.append((g, 0))
+            pass2[u] = reads
+    return pass1, pass2
+
+
+@pytest.mark.parametrize("G", [1, 2, 16])
+@pytest.mark.parametrize("W", [3, 17, 200, 2000])
+def test_grouped_reduce_consumes_every_piece_once(oracle_lib, W, G):
+    rp = np.concatenate([[0], np.cumsum([3, 0, 5000, 1, 0, 300, 12000, 7, 900, 0, 4100, 60000])])
+    rp = rp.astype(np.int64)
+    bounds = oracle_lib.partition(rp, len(rp) - 1, W, 16, 16 * 60, 256, C=5 * W)
+    stored = writer_pieces(bounds, rp)
+    pass1, pass2 = grouped_reduce(bounds, rp, G)
+    written1 = {w for _, w in pass1.values()}
+    consumed = []
+    for reads, _ in pass1.values():
+        consumed += reads
+    for u, reads in pass2.items():
+        consumed += [s for s in reads if s not in written1]
+        # group sums are read in chunk order, after the first piece
+        assert [c for c, _ in reads] == sorted(c for c, _ in reads)
+    assert sorted(consumed) == sorted(stored), "every stored piece summed exactly once"
+    for s_, u in stored.items():
+        # a group slot only ever overwrites its own leader's piece, which it reads first
+        if s_ in written1:
+            reads, w = pass1[s_[0]]
+            assert not reads or reads[0] == s_ or s_ not in reads
+    for reads, w in pass1.values():
+        assert [c for c, _ in reads] == sorted(c for c, _ in reads)
