@@ -44,10 +44,36 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="movie", help="synth config name (movie, tiny, music)")
     ap.add_argument("--f", type=int, default=None, help="rank override (rank sweep)")
-    ap.add_argument("--cpu-stride", type=int, default=8,
-                    help="oracle baseline samples every k-th row and column")
+    ap.add_argument("--cpu-flops", type=float, default=1.2e12,
+                    help="algorithmic flops of the oracle baseline's sample (every k-th row of "
+                         "each side, k chosen to match)")
+    ap.add_argument("--cpu-stride", type=int, default=0, help="fixed sampling stride instead")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
+                         "calibration), then one user and one item half-sweep; no JSON")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_herm_solve_movie_f100_traffic.txt")
+KERNEL_SRC = os.path.join(ROOT, "paper_1603_03820_amd", "csrc", "als.hip")
+
+
+def measured_traffic():
+    """HBM bytes per k_herm_solve launch from the committed counter summary, if it was taken on
+    the kernel source as it is now (else None)."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if kv.get("source_sha256") != src or "bytes_per_launch" not in kv:
+        return None
+    return float(kv["bytes_per_launch"])
 
 
 def split_rows(bounds: np.ndarray, rowptr: np.ndarray) -> int:
@@ -60,12 +86,19 @@ def split_rows(bounds: np.ndarray, rowptr: np.ndarray) -> int:
     return len(cut)
 
 
-def cpu_baseline(p, csc, stride):
-    """The fp64 oracle as it stands, on every `stride`-th row of each side, extrapolated to a
-    full half-sweep pair by the algorithmic flop count."""
+def cpu_baseline(p, csc, budget, stride=0):
+    """The fp64 oracle as it stands, on every k-th row of each side (k chosen so the sample has
+    about `budget` algorithmic flops, or `stride`), extrapolated to a full half-sweep pair by
+    the algorithmic flop count."""
     import oracle
     orc = oracle.get()
     f = p.f
+    if stride <= 0:
+        full = 0.0
+        for rp in (p.rowptr, csc[0]):
+            cnt = np.diff(rp)
+            full += float(cnt.sum() * F_h(f) + (cnt > 0).sum() * F_s(f))
+        stride = max(1, int(round(full / budget)))
     colptr, rowidx, vt = csc
     theta = p.theta0.astype(np.float64)
     xin = np.zeros((p.m, f))  # the item side's input factor: any fixed values time the same
@@ -82,7 +115,7 @@ def cpu_baseline(p, csc, stride):
         dt = time.perf_counter() - t0
         total_frac_t += dt
         total_t += dt * flops_full / flops_sample
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    threads = orc.threads()
     return {
         "value": 2.0 / total_t, "unit": "half-sweeps/s", "cores": threads, "kind": "oracle",
         "sample": f"fp64 oracle on every {stride}-th row of each side ({total_frac_t:.1f} s measured),"
@@ -112,6 +145,20 @@ def main():
     x = torch.empty((p.m, f), dtype=torch.float32, device=dev)
     rmse = torch.empty(1, dtype=torch.float64, device=dev)
     ctx = als.Context(0, max(f, 16))
+
+    if args.pmc_pass:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        driver.update_x(ctx, dp, theta, x)
+        driver.update_theta(ctx, dp, x, theta)
+        torch.cuda.synchronize()
+        print("pmc pass done", flush=True)
+        return
 
     def step():
         driver.update_x(ctx, dp, theta, x)
@@ -157,7 +204,8 @@ def main():
     roofline = {
         "kernel": f"k_herm_solve<{(f + 15) // 16}> (Gram via fp32 MFMA + in-register Cholesky)",
         "bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS,
-        "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": None,
+        "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
+        "traffic": measured_traffic(),
         "avg_launch_ms": round(herm_avg_ms, 4),
         "flops_per_launch": herm_avg_fl,
     }
@@ -196,7 +244,7 @@ def main():
         "gen_s": round(t_gen, 1),
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(p, csc, args.cpu_stride)
+        out["cpu_baseline"] = cpu_baseline(p, csc, args.cpu_flops, args.cpu_stride)
     print(json.dumps(out), flush=True)
 
 

@@ -74,7 +74,13 @@ class Oracle:
         lib.oracle_transpose.restype = ctypes.c_int
         lib.oracle_partition.argtypes = [P, i64, i64, i64, i64, i64, i64, i64, P]
         lib.oracle_partition.restype = ctypes.c_int
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         self._lib = lib
+
+    def threads(self) -> int:
+        """OpenMP threads the oracle's row loops use."""
+        return int(self._lib.oracle_threads())
 
     @staticmethod
     def _p(a):

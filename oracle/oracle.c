@@ -243,6 +243,9 @@ int oracle_transpose(const int64_t* rowptr, const int32_t* colidx, const float* 
     return ORACLE_OK;
 }
 
+/* Threads the row loops run on (OpenMP's team size for a parallel region here). */
+int oracle_threads(void) { return omp_get_max_threads(); }
+
 /*
  * The work partition of the HIP path, restated from its definition so that the library's
  * integer planning can be checked bit for bit.  Each row u costs c_row + c_nnz * n_u units
