@@ -1,0 +1,149 @@
+"""Full-size parity: the workloads at their full sizes, through the same calls bench.py times,
+against the fp64 oracle on sampled rows (each sampled x_u is recomputed from its definition) and
+on the training RMSE over every stored entry.
+
+Rows sampled per side: the longest rows (the heaviest Grams, cut into the most chunk pieces),
+random rows and empty rows.  Item-side inputs and RMSE factors are synthetic factors from the
+generator, never GPU output.  The wiki shape runs at a tenth of its rows here (same row-length
+law, column law and n); ALS_FULL_WIKI=1 runs it at 50M x 40,000 with 3.1B ratings.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import log, row_rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_1603_03820_amd import als
+    assert torch.cuda.is_available()
+    return als.Context(0, 128)
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.get()
+
+
+def sample_rows(rowptr, k_random, k_long, seed):
+    cnt = np.diff(rowptr)
+    rng = np.random.default_rng(seed)
+    longest = np.argsort(cnt, kind="stable")[-k_long:]
+    rand = rng.choice(len(cnt), size=min(k_random, len(cnt)), replace=False)
+    empty = np.flatnonzero(cnt == 0)[:5]
+    return np.unique(np.concatenate([longest, rand, empty])).astype(np.int64)
+
+
+class Side:
+    """One side of a workload: host CSR arrays and their device copies."""
+
+    def __init__(self, rowptr, colidx, vals, m, n, dev):
+        self.rowptr, self.colidx, self.vals, self.m, self.n = rowptr, colidx, vals, m, n
+        self.d = (to_dev(rowptr, dev), to_dev(colidx, dev), to_dev(vals, dev))
+
+
+def check_side(ctx, orc, side, f, lam, theta, label, k_random=600, k_long=8, seed=1):
+    from paper_1603_03820_amd import als
+    dev = ctx.device
+    log(f"{label}: half-sweep m={side.m} n={side.n} nnz={int(side.rowptr[-1])} f={f}")
+    th = to_dev(np.ascontiguousarray(theta, np.float32).reshape(side.n, f), dev)
+    x = torch.full((side.m, f), float("nan"), dtype=torch.float32, device=dev)
+    als.als_half_sweep(ctx, *side.d, side.m, side.n, f, lam, th, x)
+    torch.cuda.synchronize()
+    assert not torch.isnan(x).any().item(), f"{label}: unwritten or NaN rows"
+    assert als.als_status(ctx) == 0
+    rows = sample_rows(side.rowptr, k_random, k_long, seed)
+    xg = x[torch.from_numpy(rows).to(dev)].cpu().numpy()
+    del x, th
+    log(f"{label}: oracle on {len(rows)} sampled rows (longest {int(np.diff(side.rowptr).max())})")
+    xo, st = orc.half_sweep(side.rowptr, side.colidx, side.vals, side.m, side.n, f, lam,
+                            np.asarray(theta, np.float64).reshape(side.n, f), rows=rows)
+    assert np.all(st == 0)
+    err = row_rel_err(xg, xo)
+    worst = int(np.argmax(err))
+    log(f"{label}: max row rel err {err.max():.3e} (row {int(rows[worst])})")
+    assert err.max() <= TOL, f"{label}: row {int(rows[worst])} rel err {err.max():.3e}"
+
+
+def check_rmse(ctx, orc, side, f, x, theta, label):
+    from paper_1603_03820_amd import als
+    dev = ctx.device
+    log(f"{label}: rmse over {int(side.rowptr[-1])} entries")
+    xd = to_dev(np.ascontiguousarray(x, np.float32), dev)
+    td = to_dev(np.ascontiguousarray(theta, np.float32), dev)
+    got = float(als.als_rmse(ctx, *side.d, side.m, side.n, f, xd, td).item())
+    ref = orc.rmse(side.rowptr, side.colidx, side.vals, side.m, f, x.astype(np.float64),
+                   theta.astype(np.float64))
+    log(f"{label}: rmse gpu {got:.9f} oracle {ref:.9f}")
+    assert abs(got - ref) <= 1e-6 * max(1.0, ref)
+
+
+def load(name, f=None, m_scale=1):
+    log(f"generate {name} (f={f}, rows/{m_scale})")
+    if m_scale == 1:
+        p = synth.config(name, f=f)
+    else:
+        c = synth.CONFIGS[name]
+        p = synth.make(c["m"] // m_scale, c["n"], c["nnz"] // m_scale, rows=c["rows"],
+                       mean=c["mean"], zipf=c["zipf"], f=c["f"], lam=c["lam"], model=c["model"],
+                       seed=c["seed"], name=f"{name}/{m_scale}")
+    return p
+
+
+@pytest.fixture(scope="module")
+def movie(ctx):
+    p = load("movie")
+    colptr, rowidx, vt = p.csc()
+    return p, Side(p.rowptr, p.colidx, p.vals, p.m, p.n, ctx.device), \
+        Side(colptr, rowidx, vt, p.n, p.m, ctx.device)
+
+
+def test_movie_full_size(ctx, orc, movie):
+    p, user, item = movie
+    check_side(ctx, orc, user, p.f, p.lam, p.theta0, "movie user", seed=11)
+    xin = synth.normal(p.recipe["seed"], 8, (p.m, p.f), 0.3)
+    check_side(ctx, orc, item, p.f, p.lam, xin, "movie item", seed=12)
+    th = synth.normal(p.recipe["seed"] + 1, 8, (p.n, p.f), 0.3)
+    check_rmse(ctx, orc, user, p.f, xin, th, "movie")
+
+
+@pytest.mark.parametrize("f", [32, 64, 128])
+def test_movie_rank_sweep_full_size(ctx, orc, movie, f):
+    p, user, item = movie
+    theta0 = synth.normal(synth.RANK_SWEEP_THETA_SEED, synth.THETA0_STREAM, (p.n, f),
+                          synth.THETA0_STD)
+    check_side(ctx, orc, user, f, p.lam, theta0, f"movie f={f} user", seed=20 + f)
+    xin = synth.normal(p.recipe["seed"] + f, 8, (p.m, f), 1.0 / np.sqrt(f))
+    check_side(ctx, orc, item, f, p.lam, xin, f"movie f={f} item", seed=21 + f)
+
+
+def test_music_full_size(ctx, orc):
+    p = load("music")
+    user = Side(p.rowptr, p.colidx, p.vals, p.m, p.n, ctx.device)
+    check_side(ctx, orc, user, p.f, p.lam, p.theta0, "music user", seed=31)
+    colptr, rowidx, vt = p.csc()
+    del user
+    item = Side(colptr, rowidx, vt, p.n, p.m, ctx.device)
+    xin = synth.normal(p.recipe["seed"], 8, (p.m, p.f), 0.3)
+    check_side(ctx, orc, item, p.f, p.lam, xin, "music item", seed=32)
+
+
+def test_wiki_shape(ctx, orc):
+    scale = 1 if os.environ.get("ALS_FULL_WIKI") == "1" else 10
+    p = load("wiki", m_scale=scale)
+    user = Side(p.rowptr, p.colidx, p.vals, p.m, p.n, ctx.device)
+    check_side(ctx, orc, user, p.f, p.lam, p.theta0, f"wiki/{scale} user", seed=41)
+    colptr, rowidx, vt = p.csc()
+    del user
+    item = Side(colptr, rowidx, vt, p.n, p.m, ctx.device)
+    xin = synth.normal(p.recipe["seed"], 8, (p.m, p.f), 0.3)
+    check_side(ctx, orc, item, p.f, p.lam, xin, f"wiki/{scale} item", k_random=200, seed=42)
