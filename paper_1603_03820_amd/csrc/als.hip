@@ -160,14 +160,65 @@ constexpr int kBatchGroups = 3;
 constexpr int kBatch = 4 * kGroup * kBatchGroups;   // 48 entries
 constexpr int kRing = 2 * kBatch;
 
+// The last block column NB-1 holds f - 16 (NB-1) theta columns and the rating, the rest of it
+// padding.  In the quad form (P > 0: the theta columns fill P-1 whole column quads and the
+// rating starts quad P-1) the 16x16 tiles cover only the block columns J < NB-1, and the last
+// block column is accumulated by
+// v_mfma_f32_4x4x1_16b_f32 (16 blocks of 4x4, lane 4b + i of the A operand holds row i of block
+// b, so block b = 4e + qq is entry slot e, row quad qq of an operand block exactly as gathered):
+// q[I][p], lane 4b + j, register i holds the slot-e part of M[16 I + 4 qq + i][16 (NB-1) + 4 p + j],
+// with the second operand w[p] holding column 4p + j of the entry's last block in every quad.
+template <int NB, int P>
+struct QuadAcc {
+    f4 q[NB][P];
+};
 template <int NB>
-__device__ __forceinline__ void mfma_step(const float (&v)[NB], f4 (&acc)[ntiles(NB)]) {
+struct QuadAcc<NB, 0> {};
+
+template <int NB, int P>
+__device__ __forceinline__ void mfma_step(const float (&v)[NB], const float (&w)[P > 0 ? P : 1],
+                                          f4 (&acc)[ntiles(NB)], QuadAcc<NB, P>& qa) {
+    constexpr int JT = P > 0 ? NB - 1 : NB;   // block columns covered by 16x16 tiles
 #pragma unroll
-    for (int I = 0; I < NB; ++I)
+    for (int I = 0; I < JT; ++I)
 #pragma unroll
-        for (int J = I; J < NB; ++J)
+        for (int J = I; J < JT; ++J)
             acc[tu(NB, I, J)] =
                 __builtin_amdgcn_mfma_f32_16x16x4f32(v[I], v[J], acc[tu(NB, I, J)], 0, 0, 0);
+    if constexpr (P > 0) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I)
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+                qa.q[I][p] = __builtin_amdgcn_mfma_f32_4x4x1f32(v[I], w[p], qa.q[I][p], 0, 0, 0);
+    }
+}
+
+// The quad accumulators into standard tiles acc[tu(NB, I, NB-1)]: the tile's lane (g, c),
+// register r needs M[16 I + 4 g + r][16 (NB-1) + c] = the sum over entry slots e = 0..3, in that
+// order, of q[I][c / 4] at lane 16 e + 4 g + (c & 3), register r; columns past the quads stay 0.
+// scratch: NB * 64 vectors of LDS.
+template <int NB, int P>
+__device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc)[ntiles(NB)],
+                                              f4* scratch, int lane) {
+    const int g = lane >> 4, c = lane & 15;
+#pragma unroll
+    for (int I = 0; I < NB; ++I) acc[tu(NB, I, NB - 1)] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I) scratch[I * kWave + lane] = qa.q[I][p];
+        __syncthreads();
+        if ((c >> 2) == p) {
+            const int src = 4 * g + (c & 3);
+#pragma unroll
+            for (int I = 0; I < NB; ++I) {
+                const f4* s = scratch + I * kWave + src;
+                acc[tu(NB, I, NB - 1)] = ((s[0] + s[16]) + s[32]) + s[48];
+            }
+        }
+        __syncthreads();
+    }
 }
 
 // The theta gather of one step, as MFMA operands: lane (g, c) of block I reads
@@ -180,15 +231,19 @@ __device__ __forceinline__ void mfma_step(const float (&v)[NB], f4 (&acc)[ntiles
 //     loads are clamped to valid addresses (row 0 past the end, column 0 for padding) and the
 //     values are masked when consumed.
 // Both issue their loads unconditionally, so they stay in flight across earlier matrix ops.
-template <int NB, bool BUF>
+template <int NB, bool BUF, int P = 0>
 struct Gather;
 
-template <int NB>
-struct Gather<NB, true> {
+template <int NB, int P>
+struct Gather<NB, true, P> {
     static constexpr bool kMasked = false;
+    static constexpr int kBuf = NB + (P > 1 ? P - 1 : 0);   // operand values per step
     __amdgpu_buffer_rsrc_t rs;
     unsigned fbytes, size, lo, llast;
-    bool jr;
+    bool jr, jq;
+    // quad form: quads 0..P-2 hold theta columns 16 (NB-1) + 4p + (lane & 3) (all below f), and
+    // quad P-1 holds only the rating, in its first column (f = 16 (NB-1) + 4 (P-1))
+    unsigned lw[P > 1 ? P - 1 : 1];
     __device__ __forceinline__ Gather(const float* theta, int64_t n, int f, int c) {
         fbytes = 4u * (unsigned)f;
         size = (unsigned)n * fbytes;
@@ -198,11 +253,15 @@ struct Gather<NB, true> {
         const int jlast = 16 * (NB - 1) + c;
         llast = jlast < f ? 4u * (unsigned)jlast : size;
         jr = jlast == f;
+        jq = (c & 3) == 0;
+#pragma unroll
+        for (int p = 0; p < (P > 1 ? P - 1 : 1); ++p)
+            lw[p] = 4u * (unsigned)(16 * (NB - 1) + 4 * p + (c & 3));
     }
     __device__ __forceinline__ int word(int col, bool valid) const {
         return valid ? (int)((unsigned)col * fbytes) : (int)size;
     }
-    __device__ __forceinline__ void issue(int e, float (&v)[NB]) const {
+    __device__ __forceinline__ void issue(int e, float (&v)[kBuf]) const {
         const unsigned base = (unsigned)e + lo;
 #pragma unroll
         for (int I = 0; I < NB - 1; ++I)
@@ -210,18 +269,28 @@ struct Gather<NB, true> {
                 float, __builtin_amdgcn_raw_buffer_load_b32(rs, base + 64u * I, 0, 0));
         v[NB - 1] = __builtin_bit_cast(
             float, __builtin_amdgcn_raw_buffer_load_b32(rs, (unsigned)e + llast, 0, 0));
+#pragma unroll
+        for (int p = 0; p + 1 < P; ++p)
+            v[NB + p] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rs, (unsigned)e + lw[p], 0, 0));
     }
-    __device__ __forceinline__ void operands(const float (&B)[NB], float r, bool,
-                                             float (&v)[NB]) const {
+    __device__ __forceinline__ void operands(const float (&B)[kBuf], float r, bool,
+                                             float (&v)[NB], float (&w)[P > 0 ? P : 1]) const {
 #pragma unroll
         for (int I = 0; I < NB - 1; ++I) v[I] = B[I];
         v[NB - 1] = jr ? r : B[NB - 1];
+        if constexpr (P > 0) {
+#pragma unroll
+            for (int p = 0; p + 1 < P; ++p) w[p] = B[NB + p];
+            w[P - 1] = jq ? r : 0.f;
+        }
     }
 };
 
 template <int NB>
-struct Gather<NB, false> {
+struct Gather<NB, false, 0> {
     static constexpr bool kMasked = true;
+    static constexpr int kBuf = NB;
     const float* theta;
     int f;
     int jl[NB];
@@ -242,7 +311,7 @@ struct Gather<NB, false> {
         for (int I = 0; I < NB; ++I) v[I] = tp[jl[I]];
     }
     __device__ __forceinline__ void operands(const float (&B)[NB], float r, bool ok,
-                                             float (&v)[NB]) const {
+                                             float (&v)[NB], float (&)[1]) const {
         const float rr = ok ? r : 0.f;
 #pragma unroll
         for (int I = 0; I < NB; ++I) v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? rr : 0.f);
@@ -278,9 +347,9 @@ struct RowIndex {
 
 // The gather pipeline's in-flight state: theta values and ratings of three steps (b0..b2 at
 // the top of a group; b3 is the fourth buffer of the rotation).
-template <int NB>
+template <int NBUF>
 struct Inflight {
-    float b0[NB], b1[NB], b2[NB], b3[NB];
+    float b0[NBUF], b1[NBUF], b2[NBUF], b3[NBUF];
     float r0, r1, r2, r3;
 };
 
@@ -294,9 +363,9 @@ __device__ __forceinline__ void gram_prefetch(const G& gat, const int32_t* __res
 
 // Put a piece's first two batches into ring slots 0 and 1 (the ring must be idle) and issue
 // the gathers of its first three steps.
-template <int NB, class G>
+template <class G>
 __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, RingEntry* ring,
-                                           int lane, Inflight<NB>& in) {
+                                           int lane, Inflight<G::kBuf>& in) {
     const int g = lane >> 4;
     if (lane < kBatch) {
         ring[lane] = ix.q0;
@@ -311,11 +380,12 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
 // Accumulate entries [kbeg, kend) of one row into acc (upper block-triangle of the augmented
 // Gram matrix), starting from the state gram_stage left in the ring and in `in`.  ring: this
 // wave's LDS ring of kRing entries.  Returns with the ring idle.
-template <int NB, class G>
+template <int NB, int P, class G>
 __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
-                                          int64_t kend, f4 (&acc)[ntiles(NB)], RingEntry* ring,
-                                          int lane, Inflight<NB>& in) {
+                                          int64_t kend, f4 (&acc)[ntiles(NB)],
+                                          QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
+                                          Inflight<G::kBuf>& in) {
     const int g = lane >> 4;
     // a row has fewer than 2^31 entries (its columns are distinct int32 indices)
     const int total = (int)(kend - kbeg);
@@ -341,15 +411,15 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
         // piece's end adds zeros)
 #define ALS_SUBSTEP(B, R, BN, RN, J)                                                         \
         {                                                                                    \
-            float v[NB];                                                                     \
-            gat.operands(B, R, 4 * (s0 + (J)) + g < total, v);                               \
+            float v[NB], w[P > 0 ? P : 1];                                                   \
+            gat.operands(B, R, 4 * (s0 + (J)) + g < total, v, w);                            \
             __builtin_amdgcn_sched_barrier(0);                                               \
             int pos = rq + 4 * (J);                                                          \
             if (pos >= kRing) pos -= kRing;                                                  \
             const RingEntry e = ring[pos + g];                                               \
             RN = e.r;                                                                        \
             gat.issue(e.e, BN);                                                              \
-            mfma_step<NB>(v, acc);                                                           \
+            mfma_step<NB, P>(v, w, acc, qa);                                                 \
         }
         ALS_SUBSTEP(in.b0, in.r0, in.b3, in.r3, 0)
         ALS_SUBSTEP(in.b1, in.r1, in.b0, in.r0, 1)
@@ -626,7 +696,7 @@ struct Piece {
     bool whole;            // the chunk holds the whole row
 };
 
-template <int NB, bool BUF>
+template <int NB, bool BUF, int P>
 __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 7 ? 2 : 1)))
 void k_herm_solve(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
@@ -637,7 +707,7 @@ void k_herm_solve(
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
     __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x;
-    const Gather<NB, BUF> gat(theta, n, f, lane & 15);
+    const Gather<NB, BUF, P> gat(theta, n, f, lane & 15);
     for (;;) {
         int claim = 0;
         if (lane == 0) claim = (int)atomicAdd(chunk_ctr, 1u);
@@ -668,9 +738,9 @@ void k_herm_solve(
         Piece cur;
         if (!next_piece(u0, cur)) continue;
         RowIndex ix;
-        Inflight<NB> in;
+        Inflight<Gather<NB, BUF, P>::kBuf> in;
         gram_prefetch(gat, colidx, vals, cur.beg, cur.end, lane, ix);
-        gram_stage<NB>(gat, ix, ring, lane, in);
+        gram_stage(gat, ix, ring, lane, in);
         for (;;) {
             Piece nxt;
             const bool more = next_piece(cur.u + 1, nxt);
@@ -678,8 +748,16 @@ void k_herm_solve(
             f4 acc[ntiles(NB)];
 #pragma unroll
             for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-            gram_loop<NB>(gat, colidx, vals, cur.beg, cur.end, acc, ring, lane, in);
-            if (more) gram_stage<NB>(gat, ix, ring, lane, in);
+            QuadAcc<NB, P> qa;
+            if constexpr (P > 0) {
+#pragma unroll
+                for (int I = 0; I < NB; ++I)
+#pragma unroll
+                    for (int p = 0; p < P; ++p) qa.q[I][p] = f4{0.f, 0.f, 0.f, 0.f};
+            }
+            gram_loop<NB, P>(gat, colidx, vals, cur.beg, cur.end, acc, qa, ring, lane, in);
+            if (more) gram_stage(gat, ix, ring, lane, in);
+            if constexpr (P > 0) quad_to_tiles<NB, P>(qa, acc, reinterpret_cast<f4*>(lds.W), lane);
             // the solve is a latency-bound chain; raised priority lets it win issue slots over
             // the other wave's independent Gram MFMAs, which then fill the solve's gaps
             __builtin_amdgcn_s_setprio(2);
@@ -990,13 +1068,16 @@ Layout make_layout(const int* waves, int nb_max, int cus) {
 // form is resident at once).
 template <int NB>
 int occupancy_waves(int cus, int* waves) {
-    int blocks = 0, blocks_g = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_herm_solve<NB, true>,
-                                                                kWave, 0);
-    if (e != hipSuccess) return -1;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_g, k_herm_solve<NB, false>, kWave, 0);
-    if (e != hipSuccess) return -1;
-    if (blocks_g < blocks) blocks = blocks_g;
+    int blocks = 1 << 30;
+    const void* forms[] = {(const void*)k_herm_solve<NB, true, 0>,
+                           (const void*)k_herm_solve<NB, true, 1>,
+                           (const void*)k_herm_solve<NB, true, 2>,
+                           (const void*)k_herm_solve<NB, false, 0>};
+    for (const void* k : forms) {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, kWave, 0) != hipSuccess) return -1;
+        if (b < blocks) blocks = b;
+    }
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxWavesPerCU) blocks = kMaxWavesPerCU;
     const char* env = getenv("ALS_WAVES_PER_CU");
@@ -1116,13 +1197,28 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     hipLaunchKernelGGL(k_plan, dim3((C + 1 + 63) / 64), dim3(64), 0, st, rowptr, m, W, C,
                        (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds, chunk_ctr);
     if (ev) (void)hipEventRecord(ev[1], st);
-    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax)
-        hipLaunchKernelGGL((k_herm_solve<NB, true>), dim3(W), dim3(kWave), 0, st, rowptr, colidx,
-                           vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd, chunk_ctr);
-    else
-        hipLaunchKernelGGL((k_herm_solve<NB, false>), dim3(W), dim3(kWave), 0, st, rowptr,
+    // the quad form of the last block column: when its theta columns fill whole quads (none or
+    // one) and the rating starts a quad of its own
+    const int f_last = f - 16 * (NB - 1);
+    const int quads = (f_last == 0 || f_last == 4) ? f_last / 4 + 1 : 0;
+    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
+        if (quads == 1)
+            hipLaunchKernelGGL((k_herm_solve<NB, true, 1>), dim3(W), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
+                               chunk_ctr);
+        else if (quads == 2)
+            hipLaunchKernelGGL((k_herm_solve<NB, true, 2>), dim3(W), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
+                               chunk_ctr);
+        else
+            hipLaunchKernelGGL((k_herm_solve<NB, true, 0>), dim3(W), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
+                               chunk_ctr);
+    } else {
+        hipLaunchKernelGGL((k_herm_solve<NB, false, 0>), dim3(W), dim3(kWave), 0, st, rowptr,
                            colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
                            chunk_ctr);
+    }
     if (ev) (void)hipEventRecord(ev[2], st);
     if (C > 1) {
         // one wave per boundary: the rows' solves run side by side
