@@ -5,21 +5,25 @@
 // x_u = A_u^{-1} b_u.
 //
 // Design (one wave = one worker):
-//   k_plan          integer partition of rows (and of long rows' entries) into W equal shares
-//                   of a cost axis (see als_plan in als.h); no host synchronisation needed.
-//   k_herm_solve    per wave: walk its share row by row; gather theta_v for four entries at a
-//                   time straight into MFMA operand registers (lane = 16*k + column, so each
-//                   group of 16 lanes reads 64 contiguous bytes of one theta_v), with the rating
-//                   appended as column f, and accumulate the upper block-triangle of the
-//                   augmented Gram matrix [A b; b^T c] with v_mfma_f32_16x16x4_f32.  Rows that
-//                   end in the share are regularised and solved in registers by a blocked
-//                   Cholesky: per 16-column block, the 16 x 16 diagonal tile is factored and
-//                   inverted with lane broadcasts, and the panel and trailing updates are
-//                   again 16x16x4 MFMAs; the forward substitution rides along as the augmented
-//                   column; the back substitution is a short blocked pass.
-//   k_reduce_solve  rows cut by share boundaries: sum the per-wave partial accumulators in
-//                   wave order (fixed, so results are reproducible), then the same solve.
-//   k_rmse_*        residuals per stored entry, fp64 partial sums in a fixed order.
+//   k_plan          integer partition of the rows (and of long rows' entries) into chunks of a
+//                   cost axis: W large chunks, then 4W small ones (see als_plan in als.h); no
+//                   host synchronisation needed.
+//   k_herm_solve    persistent waves claim chunks in order and walk their row pieces; gather
+//                   theta_v for four entries at a time straight into MFMA operand registers
+//                   (lane = 16*k + column, so each group of 16 lanes reads 64 contiguous bytes of
+//                   one theta_v), with the rating appended as column f, and accumulate the upper
+//                   block-triangle of the augmented Gram matrix [A b; b^T c] with
+//                   v_mfma_f32_16x16x4_f32 (the mostly-padding last block column with 4x4x1
+//                   16-block MFMAs when it fits whole quads).  Rows that end in the chunk are
+//                   regularised and solved in registers by a blocked Cholesky: per 16-column
+//                   block, the 16 x 16 diagonal tile is factored and inverted with lane
+//                   broadcasts, and the panel and trailing updates are again 16x16x4 MFMAs; the
+//                   forward substitution rides along as the augmented column; the back
+//                   substitution is a short blocked pass.
+//   k_reduce_*      rows cut by chunk boundaries: sum the chunks' partial accumulators in chunk
+//                   order (fixed, so results are reproducible), then the same solve.
+//   k_rmse_rows     residuals per stored entry through the same gather pipeline, x_u held in
+//                   registers per row piece; fp64 partial sums in a fixed order.
 //
 // Register layout of the accumulators (the 16x16 MFMA C/D layout): tile (I,J), I <= J, lane l,
 // element r holds M[16 I + 4 (l >> 4) + r][16 J + (l & 15)] of the augmented matrix M, whose
@@ -47,7 +51,7 @@ constexpr int kTailDiv = 8;                     // the small chunks cover floor(
 constexpr int kSmallPerWave = 4;                // small chunks per wave
 constexpr int chunks_of(int waves) { return waves * (1 + kSmallPerWave); }
 constexpr int kMaxWavesPerCU = 32;
-constexpr int kRmseWavesPerCU = 24;                // RMSE: 6 waves per SIMD, latency hiding
+constexpr int kRmseWavesPerCU = 32;                // RMSE: 8 waves per SIMD, latency hiding
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
 // upper block-triangle, row-major: tile (I, J) with I <= J
@@ -377,15 +381,16 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
     q = ring[8 + g];            in.r2 = q.r;  gat.issue(q.e, in.b2);
 }
 
-// Accumulate entries [kbeg, kend) of one row into acc (upper block-triangle of the augmented
-// Gram matrix), starting from the state gram_stage left in the ring and in `in`.  ring: this
-// wave's LDS ring of kRing entries.  Returns with the ring idle.
-template <int NB, int P, class G>
-__device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
+// Run entries [kbeg, kend) of one row piece through the gather pipeline, starting from the state
+// gram_stage left in the ring and in `in`.  Per step the body takes the step's operands
+// (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
+// piece), then -- after the gather of step s + 3 has been issued -- runs the step (body.run()).
+// ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
+template <class G, class Body>
+__device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
-                                          int64_t kend, f4 (&acc)[ntiles(NB)],
-                                          QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
-                                          Inflight<G::kBuf>& in) {
+                                          int64_t kend, RingEntry* ring, int lane,
+                                          Inflight<G::kBuf>& in, Body& body) {
     const int g = lane >> 4;
     // a row has fewer than 2^31 entries (its columns are distinct int32 indices)
     const int total = (int)(kend - kbeg);
@@ -406,20 +411,18 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
         if (qb == 0 && k > 0)
             nq = load_entry(gat, colidx, vals, kbeg, total, (int64_t)(k + 1) * kBatch, lane);
         const int s0 = q * kGroup;
-        // sub-step J: issue step s0 + J + 3 into buffer BN (free: its matrix ops were issued at
-        // sub-step J - 1), then the matrix ops of step s0 + J from buffer B (a step past the
-        // piece's end adds zeros)
+        // sub-step J: issue step s0 + J + 3 into buffer BN (free: its step ran at sub-step
+        // J - 1), then run step s0 + J from buffer B (a step past the piece's end adds nothing)
 #define ALS_SUBSTEP(B, R, BN, RN, J)                                                         \
         {                                                                                    \
-            float v[NB], w[P > 0 ? P : 1];                                                   \
-            gat.operands(B, R, 4 * (s0 + (J)) + g < total, v, w);                            \
+            body.take(B, R, 4 * (s0 + (J)) + g < total);                                     \
             __builtin_amdgcn_sched_barrier(0);                                               \
             int pos = rq + 4 * (J);                                                          \
             if (pos >= kRing) pos -= kRing;                                                  \
             const RingEntry e = ring[pos + g];                                               \
             RN = e.r;                                                                        \
             gat.issue(e.e, BN);                                                              \
-            mfma_step<NB, P>(v, w, acc, qa);                                                 \
+            body.run();                                                                      \
         }
         ALS_SUBSTEP(in.b0, in.r0, in.b3, in.r3, 0)
         ALS_SUBSTEP(in.b1, in.r1, in.b0, in.r0, 1)
@@ -434,6 +437,30 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
         }
     }
     __syncthreads();   // the ring is refilled by the next piece
+}
+
+// The Gram body: accumulate the upper block-triangle of the augmented Gram matrix into acc
+// (and the quad accumulators of the last block column).
+template <int NB, int P, class G>
+struct GramBody {
+    const G& gat;
+    f4 (&acc)[ntiles(NB)];
+    QuadAcc<NB, P>& qa;
+    float v[NB], w[P > 0 ? P : 1];
+    __device__ __forceinline__ void take(const float (&B)[G::kBuf], float r, bool ok) {
+        gat.operands(B, r, ok, v, w);
+    }
+    __device__ __forceinline__ void run() { mfma_step<NB, P>(v, w, acc, qa); }
+};
+
+template <int NB, int P, class G>
+__device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
+                                          const float* __restrict__ vals, int64_t kbeg,
+                                          int64_t kend, f4 (&acc)[ntiles(NB)],
+                                          QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
+                                          Inflight<G::kBuf>& in) {
+    GramBody<NB, P, G> body{gat, acc, qa, {}, {}};
+    pipe_loop(gat, colidx, vals, kbeg, kend, ring, lane, in, body);
 }
 
 // ------------------------------------------------------------------ solve in registers ---
@@ -895,25 +922,43 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
                        threadIdx.x);
 }
 
-// RMSE pipeline shape: groups of three steps with three buffers, batches of four groups.
-constexpr int kRGroup = 3;
-constexpr int kRBatchGroups = 4;
-static_assert(4 * kRGroup * kRBatchGroups == kBatch, "RMSE batches share the ring size");
+// RMSE body: per step, entry slot g's residual r - x_u . theta_v in fp32 (the dot product over
+// the slot's 16 lanes by DPP row sums), squared and added in fp64 by the slot's first lane.  An
+// entry past the piece's end gathers zeros and rating 0, so its residual is 0.  x_u sits in
+// registers: lane (g, c) holds x_u[16 I + c] (0 past f, which also cancels the rating that the
+// gather puts in column f).
+template <int NB, class G>
+struct RmseBody {
+    const G& gat;
+    const float (&xr)[NB];
+    double& acc;
+    bool lead;
+    float v[NB], w[1], r;
+    __device__ __forceinline__ void take(const float (&B)[G::kBuf], float rr, bool ok) {
+        gat.operands(B, rr, ok, v, w);
+        r = ok ? rr : 0.f;
+    }
+    __device__ __forceinline__ void run() {
+        float d = 0.f;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) d = __builtin_fmaf(v[I], xr[I], d);
+        d = row_sum16(d);
+        const float e = r - d;
+        const double e2 = (double)e * (double)e;
+        acc += lead ? e2 : 0.0;
+    }
+};
 
-// RMSE: wave w covers entries [nnz w / W, nnz (w+1) / W); each 16-lane group takes one entry
-// per step and reads 64 contiguous bytes of theta_v and of x_u per column block, through the
-// same three-step gather pipeline as the Gram (the ring also carries each entry's row, found
-// by walking rowptr once per batch, so the pipeline runs across row boundaries).  The residual
-// is formed in fp32; squares are summed in fp64 per wave.
-template <int NB>   // NB = ceil(f / 16) column blocks
-__global__ __launch_bounds__(kWave) void k_rmse_partial(
+// RMSE partials: wave w covers entries [nnz w / W, nnz (w+1) / W), row piece by row piece through
+// the gather pipeline (the next piece's index batches load during the current piece); x_u is
+// loaded once per piece.  NB = f / 16 + 1 (the gather's block count).
+template <int NB, bool BUF>
+__global__ __launch_bounds__(kWave) void k_rmse_rows(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
-    const float* __restrict__ vals, int64_t m, int f, const float* __restrict__ x,
+    const float* __restrict__ vals, int64_t m, int64_t n, int f, const float* __restrict__ x,
     const float* __restrict__ theta, int W, double* __restrict__ partial) {
-    __shared__ int ring_c[kRing];
-    __shared__ float ring_r[kRing];
-    __shared__ int64_t ring_u[kRing];
-    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    __shared__ RingEntry ring[kRing];
+    const int lane = threadIdx.x, c = lane & 15;
     const int w = blockIdx.x;
     const int64_t nnz = rowptr[m];
     const int64_t kb = nnz / W * w + (nnz % W) * w / W;
@@ -925,93 +970,36 @@ __global__ __launch_bounds__(kWave) void k_rmse_partial(
             const int64_t mid = (lo + hi + 1) >> 1;
             if (rowptr[mid] <= kb) lo = mid; else hi = mid - 1;
         }
-        int64_t ubatch = lo;
-        int jl[NB];
-        bool jv[NB];
+        int64_t u = lo;
+        int64_t pb = kb, pe = rowptr[u + 1] < ke ? rowptr[u + 1] : ke;
+        const Gather<NB, BUF, 0> gat(theta, n, f, c);
+        RowIndex ix;
+        Inflight<Gather<NB, BUF, 0>::kBuf> in;
+        gram_prefetch(gat, colidx, vals, pb, pe, lane, ix);
+        gram_stage(gat, ix, ring, lane, in);
+        for (;;) {
+            int64_t un = u + 1;   // the next row with entries in the range
+            while (un < m && rowptr[un] < ke && rowptr[un + 1] == rowptr[un]) ++un;
+            const bool more = un < m && rowptr[un] < ke;
+            int64_t nb0 = 0, nb1 = 0;
+            if (more) {
+                nb0 = rowptr[un];
+                nb1 = rowptr[un + 1] < ke ? rowptr[un + 1] : ke;
+                gram_prefetch(gat, colidx, vals, nb0, nb1, lane, ix);
+            }
+            float xr[NB];
 #pragma unroll
-        for (int I = 0; I < NB; ++I) {
-            const int j = 16 * I + c;
-            jv[I] = j < f;
-            jl[I] = jv[I] ? j : 0;
-        }
-        const int64_t total = ke - kb;
-        const int64_t nsteps = (total + 3) >> 2;
-        const int64_t ngroups = (nsteps + kRGroup - 1) / kRGroup;
-        // one batch of entries: column, rating and row (entries past the end: row ubatch, col 0)
-        auto load_batch_rows = [&](int64_t first, int& col, float& rv, int64_t& u) {
-            col = 0;
-            rv = 0.f;
-            u = ubatch;
-            const int64_t k = kb + first + lane;
-            if (lane < kBatch && first + lane < total) {
-                col = colidx[k];
-                rv = vals[k];
-                while (rowptr[u + 1] <= k) ++u;
+            for (int I = 0; I < NB; ++I) {
+                const int j = 16 * I + c;
+                xr[I] = j < f ? x[(size_t)u * (size_t)f + j] : 0.f;
             }
-        };
-        {
-            int c0, c1;
-            float r0, r1;
-            int64_t u0, u1;
-            load_batch_rows(0, c0, r0, u0);
-            ubatch = __shfl(u0, kBatch - 1);
-            load_batch_rows(kBatch, c1, r1, u1);
-            ubatch = __shfl(u1, kBatch - 1);
-            if (lane < kBatch) {
-                ring_c[lane] = c0; ring_r[lane] = r0; ring_u[lane] = u0;
-                ring_c[kBatch + lane] = c1; ring_r[kBatch + lane] = r1; ring_u[kBatch + lane] = u1;
-            }
-            __syncthreads();
-        }
-        float t0[NB], t1[NB], t2[NB], x0[NB], x1[NB], x2[NB];
-        float r0, r1, r2;
-        auto issue = [&](int src, float (&bt)[NB], float (&bx)[NB], float& rr) {
-            const float* tp = theta + (size_t)(unsigned)ring_c[src] * (size_t)f;
-            const float* xp = x + (size_t)ring_u[src] * (size_t)f;
-            rr = ring_r[src];
-#pragma unroll
-            for (int I = 0; I < NB; ++I) { bt[I] = tp[jl[I]]; bx[I] = xp[jl[I]]; }
-        };
-        issue(0 + g, t0, x0, r0);
-        issue(4 + g, t1, x1, r1);
-        issue(8 + g, t2, x2, r2);
-        int nc = 0;
-        float nr = 0.f;
-        int64_t nu = 0;
-        for (int64_t q = 0; q < ngroups; ++q) {
-            const int qb = (int)(q % kRBatchGroups);
-            const int64_t k = q / kRBatchGroups;
-            const int cur = (int)(k & 1) * kBatch;
-            const int oth = kBatch - cur;
-            if (qb == 1 && k > 0) {
-                if (lane < kBatch) { ring_c[oth + lane] = nc; ring_r[oth + lane] = nr; ring_u[oth + lane] = nu; }
-                __syncthreads();
-            }
-            if (qb == 0 && k > 0) {
-                load_batch_rows((k + 1) * kBatch, nc, nr, nu);
-                ubatch = __shfl(nu, kBatch - 1);
-            }
-            const int nbase = (qb == kRBatchGroups - 1) ? oth : cur + (qb + 1) * kRGroup * 4;
-            const int64_t s0 = q * kRGroup;
-#define ALS_RSTEP(BT, BX, R, J)                                                              \
-            {                                                                                \
-                const bool ok = 4 * (s0 + (J)) + g < total;                                  \
-                float p = 0.f;                                                               \
-                _Pragma("unroll") for (int I = 0; I < NB; ++I)                               \
-                    p += jv[I] ? BT[I] * BX[I] : 0.f;                                        \
-                const float rr = R;                                                          \
-                __builtin_amdgcn_sched_barrier(0);                                           \
-                issue(nbase + 4 * (J) + g, BT, BX, R);                                       \
-                p = row_sum16(p);                                                            \
-                if (ok && c == 0) {                                                          \
-                    const double e = (double)(rr - p);                                       \
-                    acc += e * e;                                                            \
-                }                                                                            \
-            }
-            ALS_RSTEP(t0, x0, r0, 0)
-            ALS_RSTEP(t1, x1, r1, 1)
-            ALS_RSTEP(t2, x2, r2, 2)
-#undef ALS_RSTEP
+            RmseBody<NB, Gather<NB, BUF, 0>> body{gat, xr, acc, c == 0, {}, {}, 0.f};
+            pipe_loop(gat, colidx, vals, pb, pe, ring, lane, in, body);
+            if (!more) break;
+            gram_stage(gat, ix, ring, lane, in);
+            u = un;
+            pb = nb0;
+            pe = nb1;
         }
     }
     acc += __shfl_xor(acc, 16);
@@ -1389,14 +1377,20 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
     const int W = ctx->cus * kRmseWavesPerCU;
     double* part = (double*)(ctx->ws + ctx->lay.rmse);
     if (m > 0) {
-        switch ((f + 15) / 16) {
-#define ALS_RMSE_CASE(NBR)                                                                       \
-            case NBR:                                                                            \
-                hipLaunchKernelGGL(k_rmse_partial<NBR>, dim3(W), dim3(kWave), 0, st, rowptr,     \
-                                   colidx, vals, m, f, x, theta, W, part);                       \
+        const bool buf =
+            !ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
+        switch (f / 16 + 1) {
+#define ALS_RMSE_CASE(NB)                                                                        \
+            case NB:                                                                             \
+                if (buf)                                                                         \
+                    hipLaunchKernelGGL((k_rmse_rows<NB, true>), dim3(W), dim3(kWave), 0, st,     \
+                                       rowptr, colidx, vals, m, n, f, x, theta, W, part);        \
+                else                                                                             \
+                    hipLaunchKernelGGL((k_rmse_rows<NB, false>), dim3(W), dim3(kWave), 0, st,    \
+                                       rowptr, colidx, vals, m, n, f, x, theta, W, part);        \
                 break;
-            ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4)
-            ALS_RMSE_CASE(5) ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8)
+            ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4) ALS_RMSE_CASE(5)
+            ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8) ALS_RMSE_CASE(9)
 #undef ALS_RMSE_CASE
             default: return ALS_ERR_UNSUPPORTED_F;
         }
