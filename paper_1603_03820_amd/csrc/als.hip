@@ -641,7 +641,9 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
             if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] -= lam_n;
 
     bool ok = true;
-#pragma unroll 1
+    // unrolled: with a run-time block loop every block's results had to be copied back into the
+    // loop-carried registers (about 110 register-pair moves per row)
+#pragma unroll
     for (int K = 0; K < NB; ++K) {
         stage_diag<NB>(K, acc, S, lane);
         __syncthreads();
@@ -652,7 +654,7 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
     // back substitution, last block first; x is zero past f (b column and padding)
     for (int j = lane; j < 16 * NB; j += kWave) S.x[j] = 0.f;
     __syncthreads();
-#pragma unroll 1
+#pragma unroll
     for (int K = NB - 1; K >= 0; --K) {
         f4 part = back_matvec<NB>(K, acc, S, lane);
 #pragma unroll
