@@ -69,31 +69,26 @@ __device__ __forceinline__ float dpp_f(float v) {
         float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
-// acc + a' * b, where a' is a taken from lane N of the lane's 16-lane row (DPP row_newbcast:N)
-// folded into one v_fmac.  The caller produces `a` with neg_settled below, so the two wait states
-// a DPP source needs after its last VALU write are already there.
+// acc + a' * b, where a' is `a` taken from lane N of the lane's 16-lane row (DPP row_newbcast:N),
+// in one v_fmac.  A DPP source needs two wait states after its last VALU write; the caller keeps
+// them (volatile, so the statements stay in source order and the caller can count).  `a` may be
+// the value of `acc` itself: as an operand of its own, a copy the register allocator makes for
+// the tied accumulator never becomes the DPP source.
 template <int N>
-__device__ __forceinline__ float fmac_rowbcast(float acc, float a, float b) {
-    asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
-        : "+v"(acc)
-        : "v"(a), "v"(b), "n"(N));
+__device__ __forceinline__ float fmac_bcast(float acc, float a, float b) {
+    asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+                 : "+v"(acc)
+                 : "v"(a), "v"(b), "n"(N));
     return acc;
 }
-__device__ __forceinline__ float fmac_rowbcast_n(int n, float acc, float a, float b) {
-    switch (n) {   // n is a constant after unrolling
-#define ALS_FMAC_CASE(N) case N: return fmac_rowbcast<N>(acc, a, b);
-        ALS_FMAC_CASE(0) ALS_FMAC_CASE(1) ALS_FMAC_CASE(2) ALS_FMAC_CASE(3)
-        ALS_FMAC_CASE(4) ALS_FMAC_CASE(5) ALS_FMAC_CASE(6) ALS_FMAC_CASE(7)
-        ALS_FMAC_CASE(8) ALS_FMAC_CASE(9) ALS_FMAC_CASE(10) ALS_FMAC_CASE(11)
-        ALS_FMAC_CASE(12) ALS_FMAC_CASE(13) ALS_FMAC_CASE(14) ALS_FMAC_CASE(15)
-#undef ALS_FMAC_CASE
-    }
-    return acc;
-}
-// -v, followed by the two wait states that let a DPP operation read the result.
-__device__ __forceinline__ float neg_settled(float v) {
+// Two wait states (for a DPP read of a register a VALU op wrote just before).
+__device__ __forceinline__ void dpp_settle() { asm volatile("s_nop 1"); }
+
+// 1.0 in the lanes whose bit is set in the 64-bit lane mask, else 0 (one v_cndmask; the mask
+// is a constant in scalar registers).
+__device__ __forceinline__ float lane_select_one(uint64_t mask) {
     float r;
-    asm volatile("v_xor_b32 %0, 0x80000000, %1\n\ts_nop 1" : "=v"(r) : "v"(v));
+    asm("v_cndmask_b32_e64 %0, 0, 1.0, %1" : "=v"(r) : "s"(mask));
     return r;
 }
 
@@ -105,6 +100,30 @@ __device__ __forceinline__ float row_sum16(float v) {
     v += dpp_f<0x141>(v);   // row_half_mirror
     v += dpp_f<0x140>(v);   // row_mirror
     return v;
+}
+
+// Sum over the 16 lanes of a DPP row (lanes 16g..16g+15) of each of four values, returned to all
+// 16 lanes with the same bits: swap neighbours, swap pairs (quad_perm), then mirror within 8 and
+// within 16, each step one v_add with a DPP operand.  The four chains interleave, so each DPP
+// read sits three instructions after the write of its source.
+__device__ __forceinline__ void row_sum16x4(float& v0, float& v1, float& v2, float& v3) {
+#define ALS_ADD4(CTRL)                                                                   \
+    "v_add_f32_dpp %0, %0, %0 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
+    "v_add_f32_dpp %1, %1, %1 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
+    "v_add_f32_dpp %2, %2, %2 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
+    "v_add_f32_dpp %3, %3, %3 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
+    asm volatile("s_nop 1\n\t"
+                 ALS_ADD4("quad_perm:[1,0,3,2]")
+                 ALS_ADD4("quad_perm:[2,3,0,1]")
+                 ALS_ADD4("row_half_mirror")
+                 ALS_ADD4("row_mirror")
+                 : "+v"(v0), "+v"(v1), "+v"(v2), "+v"(v3));
+#undef ALS_ADD4
+}
+__device__ __forceinline__ void row_sum16x4(f4& v) {
+    float a = v[0], b = v[1], c = v[2], d = v[3];
+    row_sum16x4(a, b, c, d);
+    v = f4{a, b, c, d};
 }
 
 // ------------------------------------------------------------------------------- plan ----
@@ -149,20 +168,23 @@ __global__ void k_plan(const int64_t* __restrict__ rowptr, int64_t m, int W, int
 
 // --------------------------------------------------------------------- Gram + RHS --------
 
-// Gather pipeline: steps of 4 entries run in groups of kGroup = 4 steps with four operand
-// buffers; at sub-step J the theta loads of step s + 3 are issued into the buffer whose matrix
-// ops were issued at sub-step J - 1, then step s's own matrix ops run.  Every gather thus has
-// three steps of matrix work (3 * 28 MFMAs at f = 100) of this wave to hide behind, and the
-// unrolled group rotates the buffers by renaming, never by copying registers that are loading.
-// Each entry's gather word and rating come in batches of 3 groups = 48 entries through a
-// two-slot LDS ring (entry p of the piece sits at p mod 96): batch k+1 is loaded (one entry per
-// lane) at the top of batch k's first group and stored at the top of its second group, one group
-// before its first use, so any register carried around the loop only ever waits on a load older
-// than the gathers in flight.
-constexpr int kGroup = 4;
-constexpr int kBatchGroups = 3;
-constexpr int kBatch = 4 * kGroup * kBatchGroups;   // 48 entries
+// Gather pipeline: the gathers of step s + kDepth are issued before step s runs, so every gather
+// has kDepth steps of matrix work of this wave to hide behind.  Steps run in unrolled groups of
+// kGroup = kDepth + 1 with as many operand buffers; at sub-step J the step kDepth ahead goes into
+// the buffer whose step ran at sub-step J - 1, so the buffers rotate by renaming, never by copying
+// registers that are loading.  Each entry's gather word and rating come in batches of 48 entries
+// (12 steps) through a two-slot LDS ring (entry p of the piece sits at p mod 96): batch k+1 is
+// loaded (one entry per lane) at the top of batch k's first group and stored at the top of its
+// second group, before the first gather that reads it (which needs kDepth <= 5) and after the
+// last one that read the slot's previous batch, so any register carried around the loop only
+// ever waits on a load older than the gathers in flight.
+constexpr int kDepth = 3;
+constexpr int kGroup = kDepth + 1;
+constexpr int kBatch = 48;
+constexpr int kBatchGroups = kBatch / 4 / kGroup;
 constexpr int kRing = 2 * kBatch;
+static_assert(kBatchGroups * kGroup * 4 == kBatch && kBatchGroups >= 2 && 2 * kDepth <= 11,
+              "pipeline depth must divide the batch and stay within one group of lookahead");
 
 // The last block column NB-1 holds f - 16 (NB-1) theta columns and the rating, the rest of it
 // padding.  In the quad form (P > 0: the theta columns fill P-1 whole column quads and the
@@ -349,12 +371,12 @@ struct RowIndex {
     RingEntry q0, q1;
 };
 
-// The gather pipeline's in-flight state: theta values and ratings of three steps (b0..b2 at
-// the top of a group; b3 is the fourth buffer of the rotation).
+// The gather pipeline's in-flight state: operand values and ratings of the steps in flight
+// (b[0..kDepth-1] at the top of a group; b[kDepth] is the extra buffer of the rotation).
 template <int NBUF>
 struct Inflight {
-    float b0[NBUF], b1[NBUF], b2[NBUF], b3[NBUF];
-    float r0, r1, r2, r3;
+    float b[kGroup][NBUF];
+    float r[kGroup];
 };
 
 template <class G>
@@ -366,7 +388,7 @@ __device__ __forceinline__ void gram_prefetch(const G& gat, const int32_t* __res
 }
 
 // Put a piece's first two batches into ring slots 0 and 1 (the ring must be idle) and issue
-// the gathers of its first three steps.
+// the gathers of its first kDepth steps.
 template <class G>
 __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, RingEntry* ring,
                                            int lane, Inflight<G::kBuf>& in) {
@@ -376,9 +398,12 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
         ring[kBatch + lane] = ix.q1;
     }
     __syncthreads();
-    RingEntry q = ring[0 + g];  in.r0 = q.r;  gat.issue(q.e, in.b0);
-    q = ring[4 + g];            in.r1 = q.r;  gat.issue(q.e, in.b1);
-    q = ring[8 + g];            in.r2 = q.r;  gat.issue(q.e, in.b2);
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j) {
+        const RingEntry q = ring[4 * j + g];
+        in.r[j] = q.r;
+        gat.issue(q.e, in.b[j]);
+    }
 }
 
 // Run entries [kbeg, kend) of one row piece through the gather pipeline, starting from the state
@@ -386,6 +411,32 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
 // (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
 // piece), then -- after the gather of step s + 3 has been issued -- runs the step (body.run()).
 // ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
+// Sub-steps J..kGroup-1 of a group: run step s0 + J from buffer J (a step past the piece's end
+// adds nothing) after issuing step s0 + J + kDepth into buffer (J + kDepth) mod kGroup (free: its
+// step ran at sub-step J - 1).
+template <int J, class G, class Body>
+__device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* ring, int rq, int s0,
+                                              int total, int g, Inflight<G::kBuf>& in,
+                                              Body& body) {
+    if constexpr (J < kGroup) {
+        constexpr int JN = (J + kDepth) % kGroup;
+        body.take(in.b[J], in.r[J], 4 * (s0 + J) + g < total);
+        __builtin_amdgcn_sched_barrier(0);
+        int pos = rq + 4 * J;
+        if (pos >= kRing) pos -= kRing;
+        const RingEntry e = ring[pos + g];
+        in.r[JN] = e.r;
+        gat.issue(e.e, in.b[JN]);
+        body.run();
+        pipe_substeps<J + 1>(gat, ring, rq, s0, total, g, in, body);
+    }
+}
+
+// Run entries [kbeg, kend) of one row piece through the gather pipeline, starting from the state
+// gram_stage left in the ring and in `in`.  Per step the body takes the step's operands
+// (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
+// piece), then -- after the gather kDepth steps ahead has been issued -- runs the step
+// (body.run()).  ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
 template <class G, class Body>
 __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
@@ -397,38 +448,19 @@ __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restric
     const int nsteps = (total + 3) >> 2;
     const int ngroups = (nsteps + kGroup - 1) / kGroup;
     RingEntry nq{0, 0.f};
-    int qb = 0, k = 0;   // group's position in its batch; batch of the group's steps
-    int rq = 12;         // ring position of the first step issued in the group: 4 (4q + 3) mod kRing
+    int qb = 0, k = 0;       // group's position in its batch; batch of the group's steps
+    int rq = 4 * kDepth;     // ring position of the first step issued in the group
     for (int q = 0; q < ngroups; ++q) {
         // batch k+1 goes into the ring at the top of group 1, one group after its load was
         // issued at the top of group 0 (the store comes first in program order, so its wait
-        // never covers the gathers issued after the load); slot (k+1) & 1 last served batch
-        // k-1, whose final step was issued two groups earlier
+        // never covers the gathers issued after the load)
         if (qb == 1 && k > 0) {
             if (lane < kBatch) ring[((k + 1) & 1) * kBatch + lane] = nq;
             __syncthreads();
         }
         if (qb == 0 && k > 0)
             nq = load_entry(gat, colidx, vals, kbeg, total, (int64_t)(k + 1) * kBatch, lane);
-        const int s0 = q * kGroup;
-        // sub-step J: issue step s0 + J + 3 into buffer BN (free: its step ran at sub-step
-        // J - 1), then run step s0 + J from buffer B (a step past the piece's end adds nothing)
-#define ALS_SUBSTEP(B, R, BN, RN, J)                                                         \
-        {                                                                                    \
-            body.take(B, R, 4 * (s0 + (J)) + g < total);                                     \
-            __builtin_amdgcn_sched_barrier(0);                                               \
-            int pos = rq + 4 * (J);                                                          \
-            if (pos >= kRing) pos -= kRing;                                                  \
-            const RingEntry e = ring[pos + g];                                               \
-            RN = e.r;                                                                        \
-            gat.issue(e.e, BN);                                                              \
-            body.run();                                                                      \
-        }
-        ALS_SUBSTEP(in.b0, in.r0, in.b3, in.r3, 0)
-        ALS_SUBSTEP(in.b1, in.r1, in.b0, in.r0, 1)
-        ALS_SUBSTEP(in.b2, in.r2, in.b1, in.r1, 2)
-        ALS_SUBSTEP(in.b3, in.r3, in.b2, in.r2, 3)
-#undef ALS_SUBSTEP
+        pipe_substeps<0>(gat, ring, rq, q * kGroup, total, g, in, body);
         rq += 4 * kGroup;
         if (rq >= kRing) rq -= kRing;
         if (++qb == kBatchGroups) {
@@ -475,51 +507,116 @@ struct SolveLds {
     float z[16];
 };
 
-// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major).  Lane c
-// keeps column c of the Schur complement in t[] and column c of W_K = L_KK^{-1} in w[] (from
-// e_c): step kk broadcasts the pivot and column kk of L by readlane, which is also what the row
-// operations of L W = I need.  npiv real pivots; the rest of the tile is the identity.  In the
-// last block the row nlast is the augmented b row, whose L entries are y (written to S.y).
+// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major), right-looking:
+// pivot kk scales row kk of W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then
+// takes T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later
+// row i.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
+// (tr, wr: rows 4b + j); a later row 4b' + g is held by group g alone (to, wo[b']), so each
+// group updates a quarter of them.  Either way the multiplier T[i][kk] is the row's own register
+// in lane kk (DPP row_newbcast:kk), and s^2 T[kk][c], s^2 W[kk][c] are the lane's own (the
+// current block is replicated).  Between blocks the groups trade the next block's rows through
+// LDS.  Columns left of the pivot are not needed again; they go to zero as the elimination
+// proceeds instead of being masked.  npiv real pivots; later rows of W stay as the updates left
+// them (the identity in the padding).  In the last block the row nlast is the augmented b row,
+// whose L entries are y (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot
+// was positive (and not NaN) iff pmin > 0 and pmax <= the bits of +inf.
+// Registers of factor_tile (see there).
+struct FactorRegs {
+    float tr[4], wr[4], to[4], wo[4];   // to/wo[0] unused
+};
+
+// Pivot kk = 4 B + P of factor_tile.
+template <int B, int P>
+__device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin, int& pmax,
+                                             float* ystore) {
+    constexpr int kk = 4 * B + P;
+    int pb = __builtin_amdgcn_readlane(__builtin_bit_cast(int, R.tr[P]), kk);
+    pb = live ? pb : 0x3F800000;   // 1.0f
+    pmin = min(pmin, pb);
+    pmax = max(pmax, pb);
+    asm volatile("" : "+s"(pmin), "+s"(pmax));   // fold in now, in scalar registers
+    const float s = live ? __builtin_amdgcn_rsqf(__builtin_bit_cast(float, pb)) : 0.f;
+    const float ns2 = -s * s;
+    if (ystore) ystore[kk] = s * R.tr[P];   // L[nlast][kk]
+    const float at = ns2 * R.tr[P];         // -s^2 T[kk][c]
+    const float aw = ns2 * R.wr[P];         // -s^2 W[kk][c]
+    R.wr[P] *= s;                           // row kk of W is final
+    // The W updates read the T registers that the previous pivot's T updates wrote, in the same
+    // row order, so at least n - 1 instructions back for n row updates; the T updates follow the
+    // n W updates.  A block's first pivot always waits: its sources were loaded or carried over
+    // the block's branch.
+    constexpr int n = (3 - P) + (3 - B);
+    if constexpr (P == 0 || n < 3) dpp_settle();
+#pragma unroll
+    for (int j = P + 1; j < 4; ++j) R.wr[j] = fmac_bcast<kk>(R.wr[j], R.tr[j], aw);
+#pragma unroll
+    for (int bb = B + 1; bb < 4; ++bb) R.wo[bb] = fmac_bcast<kk>(R.wo[bb], R.to[bb], aw);
+#pragma unroll
+    for (int j = P + 1; j < 4; ++j) R.tr[j] = fmac_bcast<kk>(R.tr[j], R.tr[j], at);
+#pragma unroll
+    for (int bb = B + 1; bb < 4; ++bb) R.to[bb] = fmac_bcast<kk>(R.to[bb], R.to[bb], at);
+}
+
+// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major), right-looking:
+// pivot kk scales row kk of W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then
+// takes T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later
+// row i.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
+// (tr, wr: rows 4b + j); a later row 4b' + g is held by group g alone (to, wo[b']), so each
+// group updates a quarter of them.  Either way the multiplier T[i][kk] is the row's own register
+// in lane kk (DPP row_newbcast:kk), and s^2 T[kk][c], s^2 W[kk][c] are the lane's own (the
+// current block is replicated).  Between blocks the groups trade the next block's rows through
+// LDS.  Columns left of the pivot are not needed again; they go to zero as the elimination
+// proceeds instead of being masked.  npiv real pivots: a block with none is skipped (last block
+// only) and a pivot past npiv inside a block runs with s = 0, so it adds nothing (a branch per
+// pivot would make the register allocator copy DPP sources right before their reads); rows of W
+// past npiv stay as the updates left them (the identity in the padding, zero for a skipped
+// pivot).  In the last block the row nlast is the augmented b row, whose L entries are y
+// (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot was positive (and not
+// NaN) iff pmin > 0 and pmax <= the bits of +inf.
+template <int NB, int B = 0>
+__device__ __forceinline__ void factor_blocks(SolveLds<NB>& S, FactorRegs& R, int K, int npiv,
+                                              float* ystore, int& pmin, int& pmax, int lane) {
+    const int g = lane >> 4, c = lane & 15;
+    if (4 * B < npiv) {
+        factor_pivot<B, 0>(R, 4 * B + 0 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 1>(R, 4 * B + 1 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 2>(R, 4 * B + 2 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 3>(R, 4 * B + 3 < npiv, pmin, pmax, ystore);
+    }
+    if (g == 0)
+        *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * B]) = f4{R.wr[0], R.wr[1], R.wr[2], R.wr[3]};
+    if constexpr (B < 3) {
+        // rows 4(B+1) + j: group j's to/wo[B+1] -> every group's tr/wr[j].  The staged tile is
+        // in registers now; its LDS holds the exchange.
+        float* X = S.T;
+        __syncthreads();
+        *reinterpret_cast<float2*>(&X[c * 8 + 2 * g]) = float2{R.to[B + 1], R.wo[B + 1]};
+        __syncthreads();
+        const f4 u0 = *reinterpret_cast<const f4*>(&X[c * 8]);
+        const f4 u1 = *reinterpret_cast<const f4*>(&X[c * 8 + 4]);
+        R.tr[0] = u0[0]; R.wr[0] = u0[1]; R.tr[1] = u0[2]; R.wr[1] = u0[3];
+        R.tr[2] = u1[0]; R.wr[2] = u1[1]; R.tr[3] = u1[2]; R.wr[3] = u1[3];
+        factor_blocks<NB, B + 1>(S, R, K, npiv, ystore, pmin, pmax, lane);
+    }
+}
+
 template <int NB>
 __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, int nlast,
-                                            bool& ok, int lane) {
-    const int g = lane >> 4;
-    int c = lane & 15;
-    asm volatile("" : "+v"(c));   // rebuild e_c per block rather than keep 16 registers live
-    float t[16];
+                                            int& pmin, int& pmax, int lane) {
+    const int g = lane >> 4, c = lane & 15;
+    FactorRegs R;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const f4 v = *reinterpret_cast<const f4*>(&S.T[c * 16 + 4 * q]);
-        t[4 * q] = v[0]; t[4 * q + 1] = v[1]; t[4 * q + 2] = v[2]; t[4 * q + 3] = v[3];
-    }
-    const bool y_lane = (K == NB - 1) && g == 0 && c == nlast;
-    float w[16];
+    for (int j = 0; j < 4; ++j) R.tr[j] = S.T[c * 16 + j];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) w[i] = (i == c) ? 1.f : 0.f;
+    for (int bb = 1; bb < 4; ++bb) R.to[bb] = S.T[c * 16 + 4 * bb + g];
+    // identity: row j in lanes c == j; row 4b' + g in lanes 16 g + 4 b' + g
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-        if (kk < npiv) {
-            const float piv = readlane_f(t[kk], kk);
-            ok = ok && (piv > 0.f);
-            const float s = __builtin_amdgcn_rsqf(piv);
-            const float l = (c >= kk) ? t[kk] * s : 0.f;   // L[c][kk] (t is symmetric)
-            if (y_lane) S.y[16 * K + kk] = l;
-            w[kk] *= s;
-            const float nl = neg_settled(l);
-            // t[i] -= L[i][kk] L[c][kk], w[i] -= L[i][kk] w[kk]; L[i][kk] is lane i's l
+    for (int j = 0; j < 4; ++j) R.wr[j] = lane_select_one(0x0001000100010001ull << j);
 #pragma unroll
-            for (int i = kk + 1; i < 16; ++i) {
-                t[i] = fmac_rowbcast_n(i, t[i], nl, l);
-                w[i] = fmac_rowbcast_n(i, w[i], nl, w[kk]);
-            }
-        }
-    }
-    if (g == 0) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * q]) =
-                f4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
-    }
+    for (int bb = 1; bb < 4; ++bb) R.wo[bb] = lane_select_one(0x0008000400020001ull << (4 * bb));
+    R.to[0] = R.wo[0] = 0.f;
+    float* ystore = ((K == NB - 1) && lane == nlast) ? &S.y[16 * K] : nullptr;
+    factor_blocks<NB>(S, R, K, npiv, ystore, pmin, pmax, lane);
 }
 
 // Block K's acc-indexed steps, one instantiation per K (the block loop runs at run time so the
@@ -640,25 +737,25 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
         for (int r = 0; r < 4; ++r)
             if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] -= lam_n;
 
-    bool ok = true;
+    int pmin = 0x7FFFFFFF, pmax = 0;
     // unrolled: with a run-time block loop every block's results had to be copied back into the
     // loop-carried registers (about 110 register-pair moves per row)
 #pragma unroll
     for (int K = 0; K < NB; ++K) {
         stage_diag<NB>(K, acc, S, lane);
         __syncthreads();
-        factor_tile<NB>(S, K, (K < NB - 1) ? 16 : nlast, nlast, ok, lane);
+        factor_tile<NB>(S, K, (K < NB - 1) ? 16 : nlast, nlast, pmin, pmax, lane);
         __syncthreads();
         panel_update<NB>(K, acc, S, nlast, lane);
     }
+    const bool ok = pmin > 0 && pmax <= 0x7F800000;
     // back substitution, last block first; x is zero past f (b column and padding)
     for (int j = lane; j < 16 * NB; j += kWave) S.x[j] = 0.f;
     __syncthreads();
 #pragma unroll
     for (int K = NB - 1; K >= 0; --K) {
         f4 part = back_matvec<NB>(K, acc, S, lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) part[r] = row_sum16(part[r]);
+        row_sum16x4(part);
         f4 z;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -671,11 +768,9 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
         f4 xs;
 #pragma unroll
         for (int s = 0; s < 4; ++s) xs[s] = S.W[K][(4 * g + s) * 16 + c] * zc;
+        row_sum16x4(xs);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const float v = row_sum16(xs[s]);
-            xs[s] = (K < NB - 1 || 4 * g + s < nlast) ? v : 0.f;
-        }
+        for (int s = 0; s < 4; ++s) xs[s] = (K < NB - 1 || 4 * g + s < nlast) ? xs[s] : 0.f;
         if (c == 0) *reinterpret_cast<f4*>(&S.x[16 * K + 4 * g]) = xs;
         __syncthreads();
     }
