@@ -84,11 +84,11 @@ __device__ __forceinline__ float fmac_bcast(float acc, float a, float b) {
 // Two wait states (for a DPP read of a register a VALU op wrote just before).
 __device__ __forceinline__ void dpp_settle() { asm volatile("s_nop 1"); }
 
-// 1.0 in the lanes whose bit is set in the 64-bit lane mask, else 0 (one v_cndmask; the mask
+// -1.0 in the lanes whose bit is set in the 64-bit lane mask, else 0 (one v_cndmask; the mask
 // is a constant in scalar registers).
-__device__ __forceinline__ float lane_select_one(uint64_t mask) {
+__device__ __forceinline__ float lane_select_minus_one(uint64_t mask) {
     float r;
-    asm("v_cndmask_b32_e64 %0, 0, 1.0, %1" : "=v"(r) : "s"(mask));
+    asm("v_cndmask_b32_e64 %0, 0, -1.0, %1" : "=v"(r) : "s"(mask));
     return r;
 }
 
@@ -124,6 +124,33 @@ __device__ __forceinline__ void row_sum16x4(f4& v) {
     float a = v[0], b = v[1], c = v[2], d = v[3];
     row_sum16x4(a, b, c, d);
     v = f4{a, b, c, d};
+}
+
+// Sums over the 16 lanes of a DPP row of v[0..3], transposed: lane c of the row returns the sum
+// of v[c & 3] (each sum lands in four lanes, added in different orders).  Pairs of values trade
+// halves between neighbours (xor 1), then between pairs (xor 2), so every lane keeps adding one
+// value; rotations by 4 and 8 finish the sum.  11 VALU ops against 16 for four plain row sums.
+__device__ __forceinline__ float row_sum16_t(const f4& v) {
+    float x0, x1, k0, k1;
+    asm volatile(
+        "v_cndmask_b32_e64 %[x0], %[v1], %[v0], %[odd]\n\t"    // odd ? v0 : v1 (sent)
+        "v_cndmask_b32_e64 %[x1], %[v3], %[v2], %[odd]\n\t"    // odd ? v2 : v3 (sent)
+        "v_cndmask_b32_e64 %[k0], %[v0], %[v1], %[odd]\n\t"    // odd ? v1 : v0 (kept)
+        "v_cndmask_b32_e64 %[k1], %[v2], %[v3], %[odd]\n\t"    // odd ? v3 : v2 (kept)
+        "v_add_f32_dpp %[k0], %[x0], %[k0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_f32_dpp %[k1], %[x1], %[k1] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "v_cndmask_b32_e64 %[x0], %[k1], %[k0], %[two]\n\t"    // two ? k0 : k1 (sent)
+        "v_cndmask_b32_e64 %[x1], %[k0], %[k1], %[two]\n\t"    // two ? k1 : k0 (kept)
+        "s_nop 0\n\t"
+        "v_add_f32_dpp %[x1], %[x0], %[x1] quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_add_f32_dpp %[x1], %[x1], %[x1] row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_add_f32_dpp %[x1], %[x1], %[x1] row_ror:8 row_mask:0xf bank_mask:0xf"
+        : [x0] "=&v"(x0), [x1] "=&v"(x1), [k0] "=&v"(k0), [k1] "=&v"(k1)
+        : [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]),
+          [odd] "s"(0xAAAAAAAAAAAAAAAAull), [two] "s"(0xCCCCCCCCCCCCCCCCull));
+    return x1;
 }
 
 // ------------------------------------------------------------------------------- plan ----
@@ -500,26 +527,13 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
 // LDS scratch of one wave for the solve.
 template <int NB>
 struct SolveLds {
-    float W[NB][256];   // W_K = L_KK^{-1} per block, column-major: W[K][16 j + i] = W_K[i][j]
+    float W[NB][256];   // -W_K = -L_KK^{-1} per block, column-major: W[K][16 j + i] = -W_K[i][j]
     float T[256];       // a diagonal tile, row-major
     float y[16 * NB];   // forward-substitution result (row f of the augmented factor)
     float x[16 * NB];   // solution, zero past f
     float z[16];
 };
 
-// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major), right-looking:
-// pivot kk scales row kk of W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then
-// takes T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later
-// row i.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
-// (tr, wr: rows 4b + j); a later row 4b' + g is held by group g alone (to, wo[b']), so each
-// group updates a quarter of them.  Either way the multiplier T[i][kk] is the row's own register
-// in lane kk (DPP row_newbcast:kk), and s^2 T[kk][c], s^2 W[kk][c] are the lane's own (the
-// current block is replicated).  Between blocks the groups trade the next block's rows through
-// LDS.  Columns left of the pivot are not needed again; they go to zero as the elimination
-// proceeds instead of being masked.  npiv real pivots; later rows of W stay as the updates left
-// them (the identity in the padding).  In the last block the row nlast is the augmented b row,
-// whose L entries are y (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot
-// was positive (and not NaN) iff pmin > 0 and pmax <= the bits of +inf.
 // Registers of factor_tile (see there).
 struct FactorRegs {
     float tr[4], wr[4], to[4], wo[4];   // to/wo[0] unused
@@ -530,17 +544,18 @@ template <int B, int P>
 __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin, int& pmax,
                                              float* ystore) {
     constexpr int kk = 4 * B + P;
-    int pb = __builtin_amdgcn_readlane(__builtin_bit_cast(int, R.tr[P]), kk);
+    // the pivot T[kk][kk] = -N[kk][kk]: lane kk's value with the sign bit flipped (scalar)
+    int pb = __builtin_amdgcn_readlane(__builtin_bit_cast(int, R.tr[P]), kk) ^ 0x80000000;
     pb = live ? pb : 0x3F800000;   // 1.0f
     pmin = min(pmin, pb);
     pmax = max(pmax, pb);
     asm volatile("" : "+s"(pmin), "+s"(pmax));   // fold in now, in scalar registers
     const float s = live ? __builtin_amdgcn_rsqf(__builtin_bit_cast(float, pb)) : 0.f;
-    const float ns2 = -s * s;
-    if (ystore) ystore[kk] = s * R.tr[P];   // L[nlast][kk]
-    const float at = ns2 * R.tr[P];         // -s^2 T[kk][c]
-    const float aw = ns2 * R.wr[P];         // -s^2 W[kk][c]
-    R.wr[P] *= s;                           // row kk of W is final
+    const float s2 = s * s;
+    if (ystore) ystore[kk] = -s * R.tr[P];  // L[nlast][kk] = s T[kk][nlast]
+    const float at = s2 * R.tr[P];          // s^2 N[kk][c]
+    const float aw = s2 * R.wr[P];          // s^2 (-W)[kk][c]
+    R.wr[P] *= s;                           // row kk of -W is final
     // The W updates read the T registers that the previous pivot's T updates wrote, in the same
     // row order, so at least n - 1 instructions back for n row updates; the T updates follow the
     // n W updates.  A block's first pivot always waits: its sources were loaded or carried over
@@ -557,20 +572,23 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
     for (int bb = B + 1; bb < 4; ++bb) R.to[bb] = fmac_bcast<kk>(R.to[bb], R.to[bb], at);
 }
 
-// Factor and invert the symmetric 16 x 16 diagonal tile staged in S.T (row-major), right-looking:
-// pivot kk scales row kk of W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then
-// takes T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later
-// row i.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
+// Factor and invert the symmetric 16 x 16 diagonal tile T, staged negated in S.T (row-major:
+// N = -T, as the accumulator tiles hold it), right-looking: pivot kk = T[kk][kk] scales row kk of
+// W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then takes
+// T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later row i.
+// The registers hold N and -W, for which the same steps read N[i][c] += s^2 N[i][kk] N[kk][c] and
+// (-W)[i][c] += s^2 N[i][kk] (-W)[kk][c]; -W goes to S.W, as the panel and the back substitution
+// use it.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
 // (tr, wr: rows 4b + j); a later row 4b' + g is held by group g alone (to, wo[b']), so each
 // group updates a quarter of them.  Either way the multiplier T[i][kk] is the row's own register
-// in lane kk (DPP row_newbcast:kk), and s^2 T[kk][c], s^2 W[kk][c] are the lane's own (the
+// in lane kk (DPP row_newbcast:kk), and s^2 N[kk][c], s^2 (-W)[kk][c] are the lane's own (the
 // current block is replicated).  Between blocks the groups trade the next block's rows through
 // LDS.  Columns left of the pivot are not needed again; they go to zero as the elimination
 // proceeds instead of being masked.  npiv real pivots: a block with none is skipped (last block
 // only) and a pivot past npiv inside a block runs with s = 0, so it adds nothing (a branch per
 // pivot would make the register allocator copy DPP sources right before their reads); rows of W
-// past npiv stay as the updates left them (the identity in the padding, zero for a skipped
-// pivot).  In the last block the row nlast is the augmented b row, whose L entries are y
+// past npiv stay as the updates left them (the identity in the padding, zero for a pivot skipped
+// inside a block).  In the last block the row nlast is the augmented b row, whose L entries are y
 // (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot was positive (and not
 // NaN) iff pmin > 0 and pmax <= the bits of +inf.
 template <int NB, int B = 0>
@@ -609,11 +627,12 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
     for (int j = 0; j < 4; ++j) R.tr[j] = S.T[c * 16 + j];
 #pragma unroll
     for (int bb = 1; bb < 4; ++bb) R.to[bb] = S.T[c * 16 + 4 * bb + g];
-    // identity: row j in lanes c == j; row 4b' + g in lanes 16 g + 4 b' + g
+    // -identity: row j in lanes c == j; row 4b' + g in lanes 16 g + 4 b' + g
 #pragma unroll
-    for (int j = 0; j < 4; ++j) R.wr[j] = lane_select_one(0x0001000100010001ull << j);
+    for (int j = 0; j < 4; ++j) R.wr[j] = lane_select_minus_one(0x0001000100010001ull << j);
 #pragma unroll
-    for (int bb = 1; bb < 4; ++bb) R.wo[bb] = lane_select_one(0x0008000400020001ull << (4 * bb));
+    for (int bb = 1; bb < 4; ++bb)
+        R.wo[bb] = lane_select_minus_one(0x0008000400020001ull << (4 * bb));
     R.to[0] = R.wo[0] = 0.f;
     float* ystore = ((K == NB - 1) && lane == nlast) ? &S.y[16 * K] : nullptr;
     factor_blocks<NB>(S, R, K, npiv, ystore, pmin, pmax, lane);
@@ -623,7 +642,7 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
 // factor code above exists once):
 // The tiles not yet factored hold the Schur complement negated (-U), so that the trailing update
 // is a plain multiply-accumulate.
-//   stage: diagonal tile U_KK = -acc -> S.T, so that lane c can read row (= column) c;
+//   stage: diagonal tile -U_KK = acc -> S.T, so that lane c can read row (= column) c;
 //   panel: D_I = W_K U_{K,I} = L_IK^T for I > K (stored positive); y_K from the augmented
 //          column; trailing update -U_{J,I} += D_J^T D_I for K < J <= I.  Each product is four
 //          16x16x4 MFMAs over the permuted contraction index p = 4g + s, under which lane (g, c)
@@ -635,7 +654,7 @@ struct Block {
     static __device__ __forceinline__ void stage(const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
                                                  int lane) {
         const int g = lane >> 4, c = lane & 15;
-        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = -acc[tu(NB, K, K)];
+        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
     }
     static __device__ __forceinline__ void panel(f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
                                                  int nlast, int lane) {
@@ -643,7 +662,7 @@ struct Block {
             const int g = lane >> 4, c = lane & 15;
             f4 wop;   // element s: -W_K[c][4g + s] (the tiles hold -U)
 #pragma unroll
-            for (int s = 0; s < 4; ++s) wop[s] = -S.W[K][(4 * g + s) * 16 + c];
+            for (int s = 0; s < 4; ++s) wop[s] = S.W[K][(4 * g + s) * 16 + c];
 #pragma unroll
             for (int I = K + 1; I < NB; ++I) {
                 f4 d = f4{0.f, 0.f, 0.f, 0.f};
@@ -728,14 +747,21 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
                                           SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
     const int g = lane >> 4, c = lane & 15;
     const int nlast = f - 16 * (NB - 1);   // real columns of the last block; b is its column nlast
-    // -M, regularised: the factorisation below keeps unfactored tiles negated
+    // -M, regularised: the factorisation below keeps unfactored tiles negated.  The diagonal of a
+    // diagonal tile is element r of lanes c == 4g + r; in the last block only columns < nlast.
+    f4 lam, lam_last;
 #pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t) acc[t] = -acc[t];
+    for (int r = 0; r < 4; ++r) {
+        lam[r] = (c == 4 * g + r) ? lam_n : 0.f;
+        lam_last[r] = (c == 4 * g + r && c < nlast) ? lam_n : 0.f;
+    }
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            if (c == 4 * g + r && 16 * I + c < f) acc[tu(NB, I, I)][r] -= lam_n;
+        for (int J = I; J < NB; ++J) {
+            if (J > I) acc[tu(NB, I, J)] = -acc[tu(NB, I, J)];
+            else acc[tu(NB, I, I)] = -acc[tu(NB, I, I)] - (I < NB - 1 ? lam : lam_last);
+        }
 
     int pmin = 0x7FFFFFFF, pmax = 0;
     // unrolled: with a run-time block loop every block's results had to be copied back into the
@@ -749,29 +775,25 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
         panel_update<NB>(K, acc, S, nlast, lane);
     }
     const bool ok = pmin > 0 && pmax <= 0x7F800000;
-    // back substitution, last block first; x is zero past f (b column and padding)
+    // back substitution, last block first; x is zero past f (b column and padding).  Lane
+    // (g, c < 4) finishes entry kk = 4g + c of the block (the transposed row sums put it there);
+    // with -W_K in S.W, it works with -z.
     for (int j = lane; j < 16 * NB; j += kWave) S.x[j] = 0.f;
     __syncthreads();
+    const int kq = 4 * g + (c & 3);
 #pragma unroll
     for (int K = NB - 1; K >= 0; --K) {
-        f4 part = back_matvec<NB>(K, acc, S, lane);
-        row_sum16x4(part);
-        f4 z;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int kk = 4 * g + r;
-            z[r] = (K < NB - 1 || kk < nlast) ? S.y[16 * K + kk] - part[r] : 0.f;
-        }
-        if (c == 0) *reinterpret_cast<f4*>(&S.z[4 * g]) = z;
+        const bool real = K < NB - 1 || kq < nlast;
+        const float part = row_sum16_t(back_matvec<NB>(K, acc, S, lane));
+        const float nz = real ? part - S.y[16 * K + kq] : 0.f;   // -z[kq]
+        if (c < 4) S.z[kq] = nz;
         __syncthreads();
         const float zc = S.z[c];
         f4 xs;
 #pragma unroll
         for (int s = 0; s < 4; ++s) xs[s] = S.W[K][(4 * g + s) * 16 + c] * zc;
-        row_sum16x4(xs);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) xs[s] = (K < NB - 1 || 4 * g + s < nlast) ? xs[s] : 0.f;
-        if (c == 0) *reinterpret_cast<f4*>(&S.x[16 * K + 4 * g]) = xs;
+        const float xv = row_sum16_t(xs);
+        if (c < 4) S.x[16 * K + kq] = real ? xv : 0.f;
         __syncthreads();
     }
     for (int j = lane; j < f; j += kWave) xrow[j] = ok ? S.x[j] : __builtin_nanf("");
