@@ -7,6 +7,10 @@ on the CSC) and the training RMSE, all through the C ABI of include/als.h.  Inpu
 resident in HBM before the timed region.  `value` = half-sweeps per second over the K timed
 steps (2 per step).
 
+After the timed region: peak microbenchmarks (FP32 MFMA and VALU FMA rates, an HBM copy) for
+measured denominators, then the fp64 CPU oracle on a bounded row sample (all host threads, plus
+one thread on the first 10,000 user rows).
+
 Prints one JSON line.  Flop accounting (algorithmic, symmetric-half):
   per stored entry  F_h = f^2 + 3 f          (lower-triangle Gram f(f+1) + right-hand side 2f)
   per non-empty row F_s = f^3/3 + 5 f^2/2 + f/6  (Cholesky + two triangular solves)
@@ -49,6 +53,7 @@ def parse():
                          "each side, k chosen to match)")
     ap.add_argument("--cpu-stride", type=int, default=0, help="fixed sampling stride instead")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the peak microbenchmarks")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
                          "calibration), then one user and one item half-sweep; no JSON")
@@ -86,6 +91,57 @@ def split_rows(bounds: np.ndarray, rowptr: np.ndarray) -> int:
     return len(cut)
 
 
+def measure_peaks(dev):
+    """Measured FP32 MFMA and VALU FMA rates and an HBM copy rate on this GPU (the kernels in
+    csrc/peaks.hip), each the best of 3 event-timed launches on the current stream."""
+    import ctypes
+    import torch
+    from paper_1603_03820_amd import build as B
+    if not os.path.exists(B.PEAKS_LIB):
+        raise RuntimeError(f"{B.PEAKS_LIB} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(B.PEAKS_LIB)
+    V, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.peaks_mfma.argtypes = [V, V, i32, i32, V]
+    lib.peaks_fma.argtypes = [V, V, i32, i32, V]
+    lib.peaks_copy.argtypes = [V, V, i64, i32, V]
+    chains = lib.peaks_chains()
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    st = torch.cuda.current_stream()
+    sp = V(st.cuda_stream)
+    inp = torch.rand(128, device=dev)
+
+    def best(launch, work):
+        launch()
+        rates = []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            launch()
+            e1.record(st)
+            e1.synchronize()
+            rates.append(work / (e0.elapsed_time(e1) * 1e-3))
+        return max(rates)
+
+    blocks, iters = cus * 8, 20000                      # 2 waves per SIMD
+    out = torch.empty(blocks * 256, device=dev)
+    mfma = best(lambda: lib.peaks_mfma(V(inp.data_ptr()), V(out.data_ptr()), blocks, iters, sp),
+                blocks * iters * chains * 2048.0)
+    fblocks, fiters = cus * 8, 40000                    # 8 waves per SIMD
+    fout = torch.empty(fblocks * 256, device=dev)
+    fma = best(lambda: lib.peaks_fma(V(inp.data_ptr()), V(fout.data_ptr()), fblocks, fiters, sp),
+               fblocks * 256.0 * fiters * chains * 2)
+    n4 = (1 << 30) // 16                                # 1 GiB each way
+    src = torch.ones(n4 * 4, device=dev)
+    dst = torch.empty_like(src)
+    copy = best(lambda: lib.peaks_copy(V(src.data_ptr()), V(dst.data_ptr()), n4, cus * 16, sp),
+                32.0 * n4)
+    del src, dst
+    return {"mfma_f32_tflops": round(mfma / 1e12, 2), "valu_f32_fma_tflops": round(fma / 1e12, 2),
+            "hbm_copy_gbs": round(copy / 1e9, 1),
+            "mfma_clock_ghz": round(mfma / (cus * 256.0) / 1e9, 3),
+            "note": "unpacked FP32 FMA (packed FP32 is not used); copy = read + write bytes"}
+
+
 def cpu_baseline(p, csc, budget, stride=0):
     """The fp64 oracle as it stands, on every k-th row of each side (k chosen so the sample has
     about `budget` algorithmic flops, or `stride`), extrapolated to a full half-sweep pair by
@@ -103,7 +159,7 @@ def cpu_baseline(p, csc, budget, stride=0):
     theta = p.theta0.astype(np.float64)
     xin = np.zeros((p.m, f))  # the item side's input factor: any fixed values time the same
     xin[:] = 0.01
-    total_t, total_frac_t = 0.0, 0.0
+    total_t, total_frac_t, full_pair = 0.0, 0.0, 0.0
     sides = [(p.rowptr, p.colidx, p.vals, p.m, p.n, theta), (colptr, rowidx, vt, p.n, p.m, xin)]
     for rp, ci, v, m, n, th in sides:
         rows = np.arange(0, m, stride, dtype=np.int64)
@@ -115,11 +171,27 @@ def cpu_baseline(p, csc, budget, stride=0):
         dt = time.perf_counter() - t0
         total_frac_t += dt
         total_t += dt * flops_full / flops_sample
+        full_pair += flops_full
     threads = orc.threads()
+    # one core: the first 10,000 user rows on a single thread
+    k1 = min(10000, p.m)
+    rows1 = np.arange(k1, dtype=np.int64)
+    cnt = np.diff(p.rowptr)
+    fl1 = float((cnt[:k1] * F_h(f)).sum() + (cnt[:k1] > 0).sum() * F_s(f))
+    orc.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        orc.half_sweep(p.rowptr, p.colidx, p.vals, p.m, p.n, f, p.lam, theta, rows=rows1)
+        dt1 = time.perf_counter() - t0
+    finally:
+        orc.set_threads(threads)
     return {
         "value": 2.0 / total_t, "unit": "half-sweeps/s", "cores": threads, "kind": "oracle",
         "sample": f"fp64 oracle on every {stride}-th row of each side ({total_frac_t:.1f} s measured),"
                   f" extrapolated by algorithmic flops to one user + one item half-sweep",
+        "gflops": round(full_pair / total_t / 1e9, 2),
+        "one_core": {"rows": k1, "seconds": round(dt1, 2), "gflops": round(fl1 / dt1 / 1e9, 3),
+                     "sample": f"first {k1} user rows on 1 thread"},
     }
 
 
@@ -199,6 +271,7 @@ def main():
     plan_ms = np.array([pr[0] for pr in prof]).reshape(-1, 2)
     red_ms = np.array([pr[2] for pr in prof]).reshape(-1, 2)
     herm_avg_ms = float(herm_ms.mean())
+    sweep_ms = plan_ms + herm_ms + red_ms                              # per half-sweep, [step, side]
     herm_avg_fl = float(np.mean(herm_fl))
     achieved = herm_avg_fl / (herm_avg_ms * 1e-3) / 1e12
     roofline = {
@@ -236,6 +309,9 @@ def main():
                "reduce_user": round(float(red_ms[:, 0].mean()), 4),
                "reduce_item": round(float(red_ms[:, 1].mean()), 4),
                "plan": round(float(plan_ms.mean()), 4)},
+        "half_sweep_ms": {side: {"median": round(float(np.median(sweep_ms[:, k])), 4),
+                                 "min": round(float(sweep_ms[:, k].min()), 4)}
+                          for k, side in enumerate(("user", "item"))},
         "waves": {"user": W_u, "item": W_i, "chunks_user": C_u, "chunks_item": C_i,
                   "split_rows_user": split_u, "split_rows_item": split_i},
         "nonspd_rows": nonspd,
@@ -243,6 +319,10 @@ def main():
         "roofline": roofline,
         "gen_s": round(t_gen, 1),
     }
+    if not args.no_peaks:
+        out["peaks_measured"] = measure_peaks(dev)
+        roofline["frac_of_measured_mfma"] = round(
+            achieved / out["peaks_measured"]["mfma_f32_tflops"], 4)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(p, csc, args.cpu_flops, args.cpu_stride)
     print(json.dumps(out), flush=True)

@@ -76,11 +76,17 @@ class Oracle:
         lib.oracle_partition.restype = ctypes.c_int
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         self._lib = lib
 
     def threads(self) -> int:
         """OpenMP threads the oracle's row loops use."""
         return int(self._lib.oracle_threads())
+
+    def set_threads(self, n: int) -> None:
+        """Use n threads in later calls (from this thread)."""
+        self._lib.oracle_set_threads(int(n))
 
     @staticmethod
     def _p(a):

@@ -246,6 +246,9 @@ int oracle_transpose(const int64_t* rowptr, const int32_t* colidx, const float* 
 /* Threads the row loops run on (OpenMP's team size for a parallel region here). */
 int oracle_threads(void) { return omp_get_max_threads(); }
 
+/* Set that team size for later calls from this thread (timing a single core). */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+
 /*
  * The work partition of the HIP path, restated from its definition so that the library's
  * integer planning can be checked bit for bit.  Each row u costs c_row + c_nnz * n_u units

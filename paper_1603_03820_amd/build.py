@@ -34,10 +34,20 @@ def hipcc() -> str:
     return "hipcc"
 
 
+PEAKS_SRC = os.path.join(PKG, "csrc", "peaks.hip")
+PEAKS_LIB = os.path.join(PKG, "libpeaks.so")
+
+
 def build(verbose: bool = False) -> str:
-    """Compile unconditionally (the build check compiles every time) and return the path."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), SRC, "-o", tmp]
+    """Compile libals.so and the bench's peak microbenchmarks (libpeaks.so) unconditionally (the
+    build check compiles every time); return the libals.so path."""
+    _compile(PEAKS_SRC, PEAKS_LIB, verbose)
+    return _compile(SRC, LIB, verbose)
+
+
+def _compile(src: str, lib: str, verbose: bool) -> str:
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), src, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -47,8 +57,8 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

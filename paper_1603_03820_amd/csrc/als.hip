@@ -433,11 +433,6 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
     }
 }
 
-// Run entries [kbeg, kend) of one row piece through the gather pipeline, starting from the state
-// gram_stage left in the ring and in `in`.  Per step the body takes the step's operands
-// (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
-// piece), then -- after the gather of step s + 3 has been issued -- runs the step (body.run()).
-// ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
 // Sub-steps J..kGroup-1 of a group: run step s0 + J from buffer J (a step past the piece's end
 // adds nothing) after issuing step s0 + J + kDepth into buffer (J + kDepth) mod kGroup (free: its
 // step ran at sub-step J - 1).
@@ -454,7 +449,7 @@ __device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* rin
         const RingEntry e = ring[pos + g];
         in.r[JN] = e.r;
         gat.issue(e.e, in.b[JN]);
-        body.run();
+        body.template run<J>();
         pipe_substeps<J + 1>(gat, ring, rq, s0, total, g, in, body);
     }
 }
@@ -463,7 +458,8 @@ __device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* rin
 // gram_stage left in the ring and in `in`.  Per step the body takes the step's operands
 // (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
 // piece), then -- after the gather kDepth steps ahead has been issued -- runs the step
-// (body.run()).  ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
+// (body.run<J>(), J the step's place in its group of kGroup; the loop always runs whole groups).
+// ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
 template <class G, class Body>
 __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
@@ -509,6 +505,7 @@ struct GramBody {
     __device__ __forceinline__ void take(const float (&B)[G::kBuf], float r, bool ok) {
         gat.operands(B, r, ok, v, w);
     }
+    template <int J>
     __device__ __forceinline__ void run() { mfma_step<NB, P>(v, w, acc, qa); }
 };
 
@@ -1057,6 +1054,7 @@ struct RmseBody {
         gat.operands(B, rr, ok, v, w);
         r = ok ? rr : 0.f;
     }
+    template <int J>
     __device__ __forceinline__ void run() {
         float d = 0.f;
 #pragma unroll

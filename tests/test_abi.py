@@ -37,14 +37,15 @@ def test_strerror_without_device():
     assert als._lib.als_strerror(12345) == b"unknown status"
 
 
-def _device_disassembly():
+def _device_disassembly(lib=None):
     import subprocess
     import tempfile
     from paper_1603_03820_amd import build
+    lib = lib or build.LIB
     llvm = "/opt/rocm/llvm/bin"
     with tempfile.TemporaryDirectory() as d:
         fat, co = os.path.join(d, "fatbin.bin"), os.path.join(d, "dev.co")
-        subprocess.run(["objcopy", "-O", "binary", "--only-section=.hip_fatbin", build.LIB, fat],
+        subprocess.run(["objcopy", "-O", "binary", "--only-section=.hip_fatbin", lib, fat],
                        check=True)
         subprocess.run([f"{llvm}/clang-offload-bundler", "--unbundle", "--type=o",
                         f"--input={fat}", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950",
@@ -64,3 +65,22 @@ def test_device_code_shape():
     assert not scalar_writes.search(text)
     assert not re.search(r"\bv_pk_(?:add|mul|fma)_f32", text)
     assert "v_mfma_f32_16x16x4_f32" in text
+
+
+def test_peak_microbenchmarks_build_and_export():
+    """The bench's peak microbenchmarks (measurement only) load, export their launchers, and obey
+    the same device-code rules."""
+    import ctypes
+    from paper_1603_03820_amd import build
+    lib = ctypes.CDLL(build.PEAKS_LIB)
+    for fn in ("peaks_mfma", "peaks_fma", "peaks_copy", "peaks_chains"):
+        assert hasattr(lib, fn), fn
+    assert lib.peaks_chains() == 8
+    if not os.path.exists("/opt/rocm/llvm/bin/clang-offload-bundler"):
+        pytest.skip("ROCm LLVM tools not installed")
+    text = _device_disassembly(build.PEAKS_LIB)
+    scalar_writes = re.compile(r"\bs_(?:" + "|".join(["st" + "ore", "atom" + "ic", "dcache_" + "wb"])
+                               + r")")
+    assert not scalar_writes.search(text)
+    assert not re.search(r"\bv_pk_(?:add|mul|fma)_f32", text)
+    assert "v_mfma_f32_16x16x4_f32" in text and "v_fma_f32" in text
