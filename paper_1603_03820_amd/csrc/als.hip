@@ -215,22 +215,25 @@ static_assert(kBatchGroups * kGroup * 4 == kBatch && kBatchGroups >= 2 && 2 * kD
 
 // The last block column NB-1 holds f - 16 (NB-1) theta columns and the rating, the rest of it
 // padding.  In the quad form (P > 0: the theta columns fill P-1 whole column quads and the
-// rating starts quad P-1) the 16x16 tiles cover only the block columns J < NB-1, and the last
-// block column is accumulated by
-// v_mfma_f32_4x4x1_16b_f32 (16 blocks of 4x4, lane 4b + i of the A operand holds row i of block
-// b, so block b = 4e + qq is entry slot e, row quad qq of an operand block exactly as gathered):
-// q[I][p], lane 4b + j, register i holds the slot-e part of M[16 I + 4 qq + i][16 (NB-1) + 4 p + j],
-// with the second operand w[p] holding column 4p + j of the entry's last block in every quad.
+// rating is column 4 (P-1) of the block) the 16x16 tiles cover only the block columns J < NB-1.
+// The theta columns of the last block are accumulated by v_mfma_f32_4x4x1_16b_f32 (16 blocks of
+// 4x4, lane 4b + i of the A operand holds row i of block b, so block b = 4e + qq is entry slot e,
+// row quad qq of an operand block exactly as gathered): q[I][p], lane 4b + j, register i holds
+// the slot-e part of M[16 I + 4 qq + i][16 (NB-1) + 4 p + j], with the second operand w[p]
+// holding column 4p + j of the entry's last block in every quad.  The rating column needs one
+// value per row, so it is a plain FMA per lane: b[I] at lane (e, c) holds the slot-e part of
+// M[16 I + c][f] (the lane's own operand times its slot's rating).
 template <int NB, int P>
 struct QuadAcc {
-    f4 q[NB][P];
+    f4 q[NB][P > 1 ? P - 1 : 1];   // used for P > 1
+    float b[NB];
 };
 template <int NB>
 struct QuadAcc<NB, 0> {};
 
 template <int NB, int P>
 __device__ __forceinline__ void mfma_step(const float (&v)[NB], const float (&w)[P > 0 ? P : 1],
-                                          f4 (&acc)[ntiles(NB)], QuadAcc<NB, P>& qa) {
+                                          float r, f4 (&acc)[ntiles(NB)], QuadAcc<NB, P>& qa) {
     constexpr int JT = P > 0 ? NB - 1 : NB;   // block columns covered by 16x16 tiles
 #pragma unroll
     for (int I = 0; I < JT; ++I)
@@ -242,14 +245,17 @@ __device__ __forceinline__ void mfma_step(const float (&v)[NB], const float (&w)
 #pragma unroll
         for (int I = 0; I < NB; ++I)
 #pragma unroll
-            for (int p = 0; p < P; ++p)
+            for (int p = 0; p + 1 < P; ++p)
                 qa.q[I][p] = __builtin_amdgcn_mfma_f32_4x4x1f32(v[I], w[p], qa.q[I][p], 0, 0, 0);
+#pragma unroll
+        for (int I = 0; I < NB; ++I) qa.b[I] = __builtin_fmaf(v[I], r, qa.b[I]);
     }
 }
 
 // The quad accumulators into standard tiles acc[tu(NB, I, NB-1)]: the tile's lane (g, c),
 // register r needs M[16 I + 4 g + r][16 (NB-1) + c] = the sum over entry slots e = 0..3, in that
-// order, of q[I][c / 4] at lane 16 e + 4 g + (c & 3), register r; columns past the quads stay 0.
+// order, of q[I][c / 4] at lane 16 e + 4 g + (c & 3), register r, for the theta columns, and of
+// b[I] at lane 16 e + 4 g + r for the rating column; columns past it stay 0.
 // scratch: NB * 64 vectors of LDS.
 template <int NB, int P>
 __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc)[ntiles(NB)],
@@ -258,7 +264,7 @@ __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc
 #pragma unroll
     for (int I = 0; I < NB; ++I) acc[tu(NB, I, NB - 1)] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < P; ++p) {
+    for (int p = 0; p + 1 < P; ++p) {
 #pragma unroll
         for (int I = 0; I < NB; ++I) scratch[I * kWave + lane] = qa.q[I][p];
         __syncthreads();
@@ -272,6 +278,18 @@ __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc
         }
         __syncthreads();
     }
+    float* sb = reinterpret_cast<float*>(scratch);
+#pragma unroll
+    for (int I = 0; I < NB; ++I) sb[I * kWave + lane] = qa.b[I];
+    __syncthreads();
+    if (c == 4 * (P - 1)) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+            const f4* s = reinterpret_cast<const f4*>(sb + I * kWave + 4 * g);   // slot e: s[4e]
+            acc[tu(NB, I, NB - 1)] = ((s[0] + s[4]) + s[8]) + s[12];
+        }
+    }
+    __syncthreads();
 }
 
 // The theta gather of one step, as MFMA operands: lane (g, c) of block I reads
@@ -501,12 +519,13 @@ struct GramBody {
     const G& gat;
     f4 (&acc)[ntiles(NB)];
     QuadAcc<NB, P>& qa;
-    float v[NB], w[P > 0 ? P : 1];
-    __device__ __forceinline__ void take(const float (&B)[G::kBuf], float r, bool ok) {
-        gat.operands(B, r, ok, v, w);
+    float v[NB], w[P > 0 ? P : 1], r;
+    __device__ __forceinline__ void take(const float (&B)[G::kBuf], float rr, bool ok) {
+        gat.operands(B, rr, ok, v, w);
+        r = rr;   // quad form only (buffer gather: an entry past the end has rating 0)
     }
     template <int J>
-    __device__ __forceinline__ void run() { mfma_step<NB, P>(v, w, acc, qa); }
+    __device__ __forceinline__ void run() { mfma_step<NB, P>(v, w, r, acc, qa); }
 };
 
 template <int NB, int P, class G>
@@ -515,7 +534,7 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
                                           int64_t kend, f4 (&acc)[ntiles(NB)],
                                           QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
                                           Inflight<G::kBuf>& in) {
-    GramBody<NB, P, G> body{gat, acc, qa, {}, {}};
+    GramBody<NB, P, G> body{gat, acc, qa, {}, {}, 0.f};
     pipe_loop(gat, colidx, vals, kbeg, kend, ring, lane, in, body);
 }
 
@@ -536,7 +555,9 @@ struct FactorRegs {
     float tr[4], wr[4], to[4], wo[4];   // to/wo[0] unused
 };
 
-// Pivot kk = 4 B + P of factor_tile.
+// Pivot kk = 4 B + P of factor_tile.  The next pivot waits on this one's readlane, 1/piv, the
+// product for the next row and that row's update, so the next row (P + 1) is updated first and
+// 1/piv comes from its own reciprocal rather than as s^2.
 template <int B, int P>
 __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin, int& pmax,
                                              float* ystore) {
@@ -547,24 +568,30 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
     pmin = min(pmin, pb);
     pmax = max(pmax, pb);
     asm volatile("" : "+s"(pmin), "+s"(pmax));   // fold in now, in scalar registers
-    const float s = live ? __builtin_amdgcn_rsqf(__builtin_bit_cast(float, pb)) : 0.f;
-    const float s2 = s * s;
+    const float piv = __builtin_bit_cast(float, pb);
+    const float s2 = live ? __builtin_amdgcn_rcpf(piv) : 0.f;   // 1 / piv
+    const float s = live ? __builtin_amdgcn_rsqf(piv) : 0.f;    // piv^{-1/2}
+    const float at = s2 * R.tr[P];          // N[kk][c] / piv
+    const float aw = s2 * R.wr[P];          // (-W)[kk][c] / piv
     if (ystore) ystore[kk] = -s * R.tr[P];  // L[nlast][kk] = s T[kk][nlast]
-    const float at = s2 * R.tr[P];          // s^2 N[kk][c]
-    const float aw = s2 * R.wr[P];          // s^2 (-W)[kk][c]
     R.wr[P] *= s;                           // row kk of -W is final
-    // The W updates read the T registers that the previous pivot's T updates wrote, in the same
-    // row order, so at least n - 1 instructions back for n row updates; the T updates follow the
-    // n W updates.  A block's first pivot always waits: its sources were loaded or carried over
-    // the block's branch.
+    // Order: row P + 1 (W, then T: the W update reads T's column kk before the T update changes
+    // it), then the other rows' W updates, then their T updates.  A DPP read of a T register then
+    // sits at least n - 1 instructions after the previous pivot's write of it (n row updates
+    // here); a block's first pivot always waits (its sources were loaded or carried over the
+    // block's branch).
     constexpr int n = (3 - P) + (3 - B);
     if constexpr (P == 0 || n < 3) dpp_settle();
+    if constexpr (P < 3) {
+        R.wr[P + 1] = fmac_bcast<kk>(R.wr[P + 1], R.tr[P + 1], aw);
+        R.tr[P + 1] = fmac_bcast<kk>(R.tr[P + 1], R.tr[P + 1], at);
+    }
 #pragma unroll
-    for (int j = P + 1; j < 4; ++j) R.wr[j] = fmac_bcast<kk>(R.wr[j], R.tr[j], aw);
+    for (int j = P + 2; j < 4; ++j) R.wr[j] = fmac_bcast<kk>(R.wr[j], R.tr[j], aw);
 #pragma unroll
     for (int bb = B + 1; bb < 4; ++bb) R.wo[bb] = fmac_bcast<kk>(R.wo[bb], R.to[bb], aw);
 #pragma unroll
-    for (int j = P + 1; j < 4; ++j) R.tr[j] = fmac_bcast<kk>(R.tr[j], R.tr[j], at);
+    for (int j = P + 2; j < 4; ++j) R.tr[j] = fmac_bcast<kk>(R.tr[j], R.tr[j], at);
 #pragma unroll
     for (int bb = B + 1; bb < 4; ++bb) R.to[bb] = fmac_bcast<kk>(R.to[bb], R.to[bb], at);
 }
@@ -572,13 +599,13 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
 // Factor and invert the symmetric 16 x 16 diagonal tile T, staged negated in S.T (row-major:
 // N = -T, as the accumulator tiles hold it), right-looking: pivot kk = T[kk][kk] scales row kk of
 // W = L_KK^{-1} (built from the identity) by s = piv^{-1/2} and then takes
-// T[i][c] -= s^2 T[i][kk] T[kk][c] and W[i][c] -= s^2 T[i][kk] W[kk][c] for every later row i.
-// The registers hold N and -W, for which the same steps read N[i][c] += s^2 N[i][kk] N[kk][c] and
-// (-W)[i][c] += s^2 N[i][kk] (-W)[kk][c]; -W goes to S.W, as the panel and the back substitution
-// use it.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
+// T[i][c] -= T[i][kk] T[kk][c] / piv and W[i][c] -= T[i][kk] W[kk][c] / piv for every later row i.
+// The registers hold N and -W, for which the same steps read N[i][c] += N[i][kk] N[kk][c] / piv
+// and (-W)[i][c] += N[i][kk] (-W)[kk][c] / piv; -W goes to S.W, as the panel and the back
+// substitution use it.  Lane (g, c) holds column c.  The rows of the current 4-row block b sit in every group
 // (tr, wr: rows 4b + j); a later row 4b' + g is held by group g alone (to, wo[b']), so each
 // group updates a quarter of them.  Either way the multiplier T[i][kk] is the row's own register
-// in lane kk (DPP row_newbcast:kk), and s^2 N[kk][c], s^2 (-W)[kk][c] are the lane's own (the
+// in lane kk (DPP row_newbcast:kk), and N[kk][c] / piv, (-W)[kk][c] / piv are the lane's own (the
 // current block is replicated).  Between blocks the groups trade the next block's rows through
 // LDS.  Columns left of the pivot are not needed again; they go to zero as the elimination
 // proceeds instead of being masked.  npiv real pivots: a block with none is skipped (last block
@@ -894,9 +921,11 @@ void k_herm_solve(
             QuadAcc<NB, P> qa;
             if constexpr (P > 0) {
 #pragma unroll
-                for (int I = 0; I < NB; ++I)
+                for (int I = 0; I < NB; ++I) {
 #pragma unroll
-                    for (int p = 0; p < P; ++p) qa.q[I][p] = f4{0.f, 0.f, 0.f, 0.f};
+                    for (int p = 0; p + 1 < P; ++p) qa.q[I][p] = f4{0.f, 0.f, 0.f, 0.f};
+                    qa.b[I] = 0.f;
+                }
             }
             gram_loop<NB, P>(gat, colidx, vals, cur.beg, cur.end, acc, qa, ring, lane, in);
             if (more) gram_stage(gat, ix, ring, lane, in);
