@@ -555,9 +555,9 @@ struct FactorRegs {
     float tr[4], wr[4], to[4], wo[4];   // to/wo[0] unused
 };
 
-// Pivot kk = 4 B + P of factor_tile.  The next pivot waits on this one's readlane, 1/piv, the
-// product for the next row and that row's update, so the next row (P + 1) is updated first and
-// 1/piv comes from its own reciprocal rather than as s^2.
+// Pivot kk = 4 B + P of factor_tile.  The next pivot waits on this one's readlane, s, s^2, the
+// product for the next row and that row's update, so the next row (P + 1) is updated first.
+// One transcendental per pivot (s = piv^{-1/2}; 1/piv = s^2).
 template <int B, int P>
 __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin, int& pmax,
                                              float* ystore) {
@@ -568,9 +568,8 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
     pmin = min(pmin, pb);
     pmax = max(pmax, pb);
     asm volatile("" : "+s"(pmin), "+s"(pmax));   // fold in now, in scalar registers
-    const float piv = __builtin_bit_cast(float, pb);
-    const float s2 = live ? __builtin_amdgcn_rcpf(piv) : 0.f;   // 1 / piv
-    const float s = live ? __builtin_amdgcn_rsqf(piv) : 0.f;    // piv^{-1/2}
+    const float s = live ? __builtin_amdgcn_rsqf(__builtin_bit_cast(float, pb)) : 0.f;
+    const float s2 = s * s;   // 1 / piv
     const float at = s2 * R.tr[P];          // N[kk][c] / piv
     const float aw = s2 * R.wr[P];          // (-W)[kk][c] / piv
     if (ystore) ystore[kk] = -s * R.tr[P];  // L[nlast][kk] = s T[kk][nlast]
