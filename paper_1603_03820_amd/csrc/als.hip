@@ -51,7 +51,7 @@ constexpr int kTailDiv = 8;                     // the small chunks cover floor(
 constexpr int kSmallPerWave = 4;                // small chunks per wave
 constexpr int chunks_of(int waves) { return waves * (1 + kSmallPerWave); }
 constexpr int kMaxWavesPerCU = 32;
-constexpr int kRmseWavesPerCU = 32;                // RMSE: 8 waves per SIMD, latency hiding
+constexpr int kRmseWavesPerCU = 32;                // RMSE: up to 8 waves per SIMD (occupancy)
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
 // upper block-triangle, row-major: tile (I, J) with I <= J
@@ -130,27 +130,27 @@ __device__ __forceinline__ void row_sum16x4(f4& v) {
 // of v[c & 3] (each sum lands in four lanes, added in different orders).  Pairs of values trade
 // halves between neighbours (xor 1), then between pairs (xor 2), so every lane keeps adding one
 // value; rotations by 4 and 8 finish the sum.  11 VALU ops against 16 for four plain row sums.
-__device__ __forceinline__ float row_sum16_t(const f4& v) {
-    float x0, x1, k0, k1;
+__device__ __forceinline__ float row_sum16_t(f4 v) {
+    float v0 = v[0], v1 = v[1], v2 = v[2], v3 = v[3], t0, t1;
     asm volatile(
-        "v_cndmask_b32_e64 %[x0], %[v1], %[v0], %[odd]\n\t"    // odd ? v0 : v1 (sent)
-        "v_cndmask_b32_e64 %[x1], %[v3], %[v2], %[odd]\n\t"    // odd ? v2 : v3 (sent)
-        "v_cndmask_b32_e64 %[k0], %[v0], %[v1], %[odd]\n\t"    // odd ? v1 : v0 (kept)
-        "v_cndmask_b32_e64 %[k1], %[v2], %[v3], %[odd]\n\t"    // odd ? v3 : v2 (kept)
-        "v_add_f32_dpp %[k0], %[x0], %[k0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
-        "v_add_f32_dpp %[k1], %[x1], %[k1] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
-        "v_cndmask_b32_e64 %[x0], %[k1], %[k0], %[two]\n\t"    // two ? k0 : k1 (sent)
-        "v_cndmask_b32_e64 %[x1], %[k0], %[k1], %[two]\n\t"    // two ? k1 : k0 (kept)
+        "v_cndmask_b32_e64 %[t0], %[v1], %[v0], %[odd]\n\t"    // odd ? v0 : v1 (sent)
+        "v_cndmask_b32_e64 %[t1], %[v3], %[v2], %[odd]\n\t"    // odd ? v2 : v3 (sent)
+        "v_cndmask_b32_e64 %[v0], %[v0], %[v1], %[odd]\n\t"    // odd ? v1 : v0 (kept)
+        "v_cndmask_b32_e64 %[v2], %[v2], %[v3], %[odd]\n\t"    // odd ? v3 : v2 (kept)
+        "v_add_f32_dpp %[v0], %[t0], %[v0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_f32_dpp %[v2], %[t1], %[v2] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "v_cndmask_b32_e64 %[t0], %[v2], %[v0], %[two]\n\t"    // two ? v0 : v2 (sent)
+        "v_cndmask_b32_e64 %[v0], %[v0], %[v2], %[two]\n\t"    // two ? v2 : v0 (kept)
         "s_nop 0\n\t"
-        "v_add_f32_dpp %[x1], %[x0], %[x1] quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_f32_dpp %[v0], %[t0], %[v0] quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
         "s_nop 1\n\t"
-        "v_add_f32_dpp %[x1], %[x1], %[x1] row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_f32_dpp %[v0], %[v0], %[v0] row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
         "s_nop 1\n\t"
-        "v_add_f32_dpp %[x1], %[x1], %[x1] row_ror:8 row_mask:0xf bank_mask:0xf"
-        : [x0] "=&v"(x0), [x1] "=&v"(x1), [k0] "=&v"(k0), [k1] "=&v"(k1)
-        : [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]),
-          [odd] "s"(0xAAAAAAAAAAAAAAAAull), [two] "s"(0xCCCCCCCCCCCCCCCCull));
-    return x1;
+        "v_add_f32_dpp %[v0], %[v0], %[v0] row_ror:8 row_mask:0xf bank_mask:0xf"
+        : [t0] "=&v"(t0), [t1] "=&v"(t1), [v0] "+v"(v0), [v1] "+v"(v1), [v2] "+v"(v2),
+          [v3] "+v"(v3)
+        : [odd] "s"(0xAAAAAAAAAAAAAAAAull), [two] "s"(0xCCCCCCCCCCCCCCCCull));
+    return v0;
 }
 
 // ------------------------------------------------------------------------------- plan ----
@@ -665,7 +665,8 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
 // factor code above exists once):
 // The tiles not yet factored hold the Schur complement negated (-U), so that the trailing update
 // is a plain multiply-accumulate.
-//   stage: diagonal tile -U_KK = acc -> S.T, so that lane c can read row (= column) c;
+//   stage: diagonal tile -U_KK = acc, less lambda n_u on its diagonal (real columns only),
+//          -> S.T, so that lane c can read row (= column) c;
 //   panel: D_I = W_K U_{K,I} = L_IK^T for I > K (stored positive); y_K from the augmented
 //          column; trailing update -U_{J,I} += D_J^T D_I for K < J <= I.  Each product is four
 //          16x16x4 MFMAs over the permuted contraction index p = 4g + s, under which lane (g, c)
@@ -675,9 +676,14 @@ __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, in
 template <int NB, int K>
 struct Block {
     static __device__ __forceinline__ void stage(const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
-                                                 int lane) {
+                                                 float lam_n, int nlast, int lane) {
         const int g = lane >> 4, c = lane & 15;
-        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = acc[tu(NB, K, K)];
+        f4 t = acc[tu(NB, K, K)];
+        // the diagonal is element r of lanes c == 4g + r
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (c == 4 * g + r && (K < NB - 1 || c < nlast)) t[r] -= lam_n;
+        *reinterpret_cast<f4*>(&S.T[c * 16 + 4 * g]) = t;
     }
     static __device__ __forceinline__ void panel(f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
                                                  int nlast, int lane) {
@@ -728,12 +734,12 @@ __device__ __forceinline__ void case_marker() {
 }
 template <int NB, int K = 0>
 __device__ __forceinline__ void stage_diag(int k, const f4 (&acc)[ntiles(NB)], SolveLds<NB>& S,
-                                           int lane) {
+                                           float lam_n, int nlast, int lane) {
     if (k == K) {
-        Block<NB, K>::stage(acc, S, lane);
+        Block<NB, K>::stage(acc, S, lam_n, nlast, lane);
         case_marker<K>();
     } else if constexpr (K + 1 < NB) {
-        stage_diag<NB, K + 1>(k, acc, S, lane);
+        stage_diag<NB, K + 1>(k, acc, S, lam_n, nlast, lane);
     }
 }
 template <int NB, int K = 0>
@@ -770,28 +776,17 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
                                           SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
     const int g = lane >> 4, c = lane & 15;
     const int nlast = f - 16 * (NB - 1);   // real columns of the last block; b is its column nlast
-    // -M, regularised: the factorisation below keeps unfactored tiles negated.  The diagonal of a
-    // diagonal tile is element r of lanes c == 4g + r; in the last block only columns < nlast.
-    f4 lam, lam_last;
+    // -M: the factorisation below keeps unfactored tiles negated (the regularisation joins each
+    // diagonal tile as it is staged)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        lam[r] = (c == 4 * g + r) ? lam_n : 0.f;
-        lam_last[r] = (c == 4 * g + r && c < nlast) ? lam_n : 0.f;
-    }
-#pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int J = I; J < NB; ++J) {
-            if (J > I) acc[tu(NB, I, J)] = -acc[tu(NB, I, J)];
-            else acc[tu(NB, I, I)] = -acc[tu(NB, I, I)] - (I < NB - 1 ? lam : lam_last);
-        }
+    for (int t = 0; t < ntiles(NB); ++t) acc[t] = -acc[t];
 
     int pmin = 0x7FFFFFFF, pmax = 0;
     // unrolled: with a run-time block loop every block's results had to be copied back into the
     // loop-carried registers (about 110 register-pair moves per row)
 #pragma unroll
     for (int K = 0; K < NB; ++K) {
-        stage_diag<NB>(K, acc, S, lane);
+        stage_diag<NB>(K, acc, S, lam_n, nlast, lane);
         __syncthreads();
         factor_tile<NB>(S, K, (K < NB - 1) ? 16 : nlast, nlast, pmin, pmax, lane);
         __syncthreads();
@@ -866,7 +861,7 @@ struct Piece {
 };
 
 template <int NB, bool BUF, int P>
-__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 7 ? 2 : 1)))
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 8 ? 2 : 1)))
 void k_herm_solve(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int64_t n,
@@ -1102,6 +1097,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, int64_t m, int64_t n, int f, const float* __restrict__ x,
     const float* __restrict__ theta, int W, double* __restrict__ partial) {
+    using G = Gather<NB, BUF, 0>;
     __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x, c = lane & 15;
     const int w = blockIdx.x;
@@ -1117,9 +1113,9 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
         }
         int64_t u = lo;
         int64_t pb = kb, pe = rowptr[u + 1] < ke ? rowptr[u + 1] : ke;
-        const Gather<NB, BUF, 0> gat(theta, n, f, c);
+        const G gat(theta, n, f, c);
         RowIndex ix;
-        Inflight<Gather<NB, BUF, 0>::kBuf> in;
+        Inflight<G::kBuf> in;
         gram_prefetch(gat, colidx, vals, pb, pe, lane, ix);
         gram_stage(gat, ix, ring, lane, in);
         for (;;) {
@@ -1138,7 +1134,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
                 const int j = 16 * I + c;
                 xr[I] = j < f ? x[(size_t)u * (size_t)f + j] : 0.f;
             }
-            RmseBody<NB, Gather<NB, BUF, 0>> body{gat, xr, acc, c == 0, {}, {}, 0.f};
+            RmseBody<NB, G> body{gat, xr, acc, c == 0, {}, {}, 0.f};
             pipe_loop(gat, colidx, vals, pb, pe, ring, lane, in, body);
             if (!more) break;
             gram_stage(gat, ix, ring, lane, in);
@@ -1217,6 +1213,23 @@ int occupancy_waves(int cus, int* waves) {
     if (env && atoi(env) > 0) blocks = atoi(env) < blocks ? atoi(env) : blocks;
     *waves = blocks * cus;
     return 0;
+}
+
+// Launch the RMSE partials kernel with as many resident waves as it fits, up to
+// kRmseWavesPerCU per CU (the partials buffer holds that many); *W gets the wave count.
+template <int NB, bool BUF>
+hipError_t rmse_rows_launch(int cus, hipStream_t st, const int64_t* rowptr,
+                            const int32_t* colidx, const float* vals, int64_t m, int64_t n,
+                            int f, const float* x, const float* theta, double* part, int* W) {
+    int b = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &b, (const void*)k_rmse_rows<NB, BUF>, kWave, 0);
+    if (e != hipSuccess) return e;
+    b = b < 1 ? 1 : (b > kRmseWavesPerCU ? kRmseWavesPerCU : b);
+    *W = cus * b;
+    hipLaunchKernelGGL((k_rmse_rows<NB, BUF>), dim3(*W), dim3(kWave), 0, st, rowptr, colidx,
+                       vals, m, n, f, x, theta, *W, part);
+    return hipGetLastError();
 }
 
 int waves_for_nb(int nb, int cus, int* w) {
@@ -1519,26 +1532,26 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
     hipStream_t st = (hipStream_t)stream;
-    const int W = ctx->cus * kRmseWavesPerCU;
+    int W = 0;
     double* part = (double*)(ctx->ws + ctx->lay.rmse);
+    hipError_t le = hipSuccess;
     if (m > 0) {
         const bool buf =
             !ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
+#define ALS_RMSE_ARGS ctx->cus, st, rowptr, colidx, vals, m, n, f, x, theta, part, &W
         switch (f / 16 + 1) {
-#define ALS_RMSE_CASE(NB)                                                                        \
-            case NB:                                                                             \
-                if (buf)                                                                         \
-                    hipLaunchKernelGGL((k_rmse_rows<NB, true>), dim3(W), dim3(kWave), 0, st,     \
-                                       rowptr, colidx, vals, m, n, f, x, theta, W, part);        \
-                else                                                                             \
-                    hipLaunchKernelGGL((k_rmse_rows<NB, false>), dim3(W), dim3(kWave), 0, st,    \
-                                       rowptr, colidx, vals, m, n, f, x, theta, W, part);        \
+#define ALS_RMSE_CASE(NB)                                                           \
+            case NB:                                                                \
+                le = buf ? rmse_rows_launch<NB, true>(ALS_RMSE_ARGS)                \
+                         : rmse_rows_launch<NB, false>(ALS_RMSE_ARGS);              \
                 break;
             ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4) ALS_RMSE_CASE(5)
             ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8) ALS_RMSE_CASE(9)
 #undef ALS_RMSE_CASE
+#undef ALS_RMSE_ARGS
             default: return ALS_ERR_UNSUPPORTED_F;
         }
+        if (le != hipSuccess) return fail_hip(ctx, le);
     }
     hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? W : 0, part,
                        rmse_out);

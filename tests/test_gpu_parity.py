@@ -253,20 +253,24 @@ def test_argument_errors(ctx):
     assert rc == -4
 
 
-def test_rmse_matches_oracle(ctx, orc):
+@pytest.mark.parametrize("form", ["buffer", "global"])
+def test_rmse_matches_oracle(ctx, ctx_global, orc, form):
+    """Both gather forms of the RMSE (buffer loads, 64-bit global loads), at widths that end a
+    block exactly, inside a block and one past a block."""
     from paper_1603_03820_amd import als
-    for f in (7, 100, 128):
+    c = ctx if form == "buffer" else ctx_global
+    for f in (4, 7, 33, 100, 124, 128):
         p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
-                       plant_f=16, seed=31)
+                       plant_f=min(f, 16), seed=31)
         x = synthetic_factor(p.m, f, 32, 0.3)
         th = synthetic_factor(p.n, f, 33, 0.3)
-        log(f"rmse f={f}")
-        dev = ctx.device
-        out = als.als_rmse(ctx, to_dev(p.rowptr, dev), to_dev(p.colidx, dev),
+        log(f"rmse {form} f={f}")
+        dev = c.device
+        out = als.als_rmse(c, to_dev(p.rowptr, dev), to_dev(p.colidx, dev),
                            to_dev(p.vals, dev), p.m, p.n, f, to_dev(x, dev), to_dev(th, dev))
         ref = orc.rmse(p.rowptr, p.colidx, p.vals, p.m, f, x.astype(np.float64),
                        th.astype(np.float64))
-        assert abs(out.item() - ref) <= 1e-6 * ref
+        assert abs(out.item() - ref) <= 1e-6 * ref, (form, f, out.item(), ref)
 
 
 def test_tiny_trajectory_ten_iterations(ctx, orc):
