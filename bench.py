@@ -54,6 +54,12 @@ def parse():
     ap.add_argument("--cpu-stride", type=int, default=0, help="fixed sampling stride instead")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-peaks", action="store_true", help="skip the peak microbenchmarks")
+    ap.add_argument("--driver", action="store_true",
+                    help="instead of the step benchmark: the ALS driver on a seeded 99/1 "
+                         "train/test split, test RMSE per iteration, with and without async "
+                         "checkpoints (one JSON line)")
+    ap.add_argument("--test-frac", type=float, default=0.01)
+    ap.add_argument("--checkpoint-every", type=int, default=5)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
                          "calibration), then one user and one item half-sweep; no JSON")
@@ -195,12 +201,65 @@ def cpu_baseline(p, csc, budget, stride=0):
     }
 
 
+def driver_bench(args):
+    """The driver (test RMSE per iteration, async checkpoints) on the workload's training split."""
+    import shutil
+    import tempfile
+    import torch
+    import synth
+    from paper_1603_03820_amd import als, driver
+
+    dev = torch.device("cuda", 0)
+    p = synth.config(args.config, f=args.f)
+    (tr, te) = synth.split(p.rowptr, p.colidx, p.vals, args.test_frac, p.recipe["seed"])
+    csc = synth.transpose(p.m, p.n, *tr)
+    dp = driver.DeviceProblem.from_host(p.m, p.n, p.f, p.lam, *tr, *csc, dev)
+    test = driver.RatingSet.from_host(p.m, p.n, *te, dev)
+    ctx = als.Context(0, max(p.f, 16))
+    th0 = torch.from_numpy(p.theta0).to(dev)
+    iters = args.steps
+    driver.run(ctx, dp, th0, args.warmup, test=test)             # warm-up
+    _, _, plain = driver.run(ctx, dp, th0, iters, test=test)
+    tmp = tempfile.mkdtemp(prefix="als_ckpt_")
+    try:
+        ck = driver.AsyncCheckpointer(tmp, torch.empty((p.m, p.f), device=dev), th0)
+        t0 = time.perf_counter()
+        _, _, with_ck = driver.run(ctx, dp, th0, iters, test=test, checkpointer=ck,
+                                   checkpoint_every=args.checkpoint_every)
+        t_ck = time.perf_counter() - t0
+        files = list(ck.saved)
+        ck_bytes = 4 * (p.m + p.n) * p.f
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    wall = plain[-1]["wall_s"]
+    out = {
+        "metric": "ALS iterations/s with training and held-out test RMSE per iteration",
+        "value": round(iters / wall, 3), "unit": "iterations/s", "n_gpus": 1, "steps": iters,
+        "warmup": args.warmup, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{p.name} training split: m={p.m} n={p.n} "
+                               f"nnz={int(tr[0][-1])} (test {int(te[0][-1])}) f={p.f} "
+                               f"lambda={p.lam}", "test_frac": args.test_frac},
+        "curve": [{k: (round(v, 6) if isinstance(v, float) else v) for k, v in h.items()}
+                  for h in plain],
+        "checkpoint": {"every": args.checkpoint_every, "files": len(files),
+                       "bytes_each": ck_bytes,
+                       "wall_s_with": round(t_ck, 4), "wall_s_without": round(wall, 4),
+                       "overhead_ms_per_iteration": round((t_ck - wall) / iters * 1e3, 3),
+                       "same_rmse": [h["test_rmse"] for h in with_ck] ==
+                                    [h["test_rmse"] for h in plain]},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.driver:
+        driver_bench(args)
+        return
     import torch
     import synth
     from paper_1603_03820_amd import als, driver

@@ -45,6 +45,7 @@ _MODELS = {"tiny": 0, "movie": 1, "music": 2, "wiki": 3}
 _ROWS = {"uniform": 0, "lognormal": 1}
 THETA0_STREAM = 7
 THETA0_STD = 0.01
+SPLIT_STREAM = 9   # held-out test split (stream 8 draws test factors)
 
 
 def build(force: bool = False) -> str:
@@ -73,8 +74,9 @@ def _load():
         lib.synth_normal.argtypes = [u64, u32, i64, dbl, P]
         lib.synth_transpose.argtypes = [i64, i64, P, P, P, P, P, P]
         lib.synth_philox4x32_10.argtypes = [P, P, P]
+        lib.synth_split_mask.argtypes = [u64, u32, i64, u32, P]
         for fn in ("synth_row_counts", "synth_columns", "synth_values", "synth_normal",
-                   "synth_transpose"):
+                   "synth_transpose", "synth_split_mask"):
             getattr(lib, fn).restype = ctypes.c_int
         lib.synth_philox4x32_10.restype = None
         _lib = lib
@@ -150,6 +152,33 @@ def normal(seed: int, stream: int, shape, std: float):
     out = np.empty(shape, dtype=np.float32)
     _check(_load().synth_normal(seed, stream, out.size, std, _ptr(out)), "normal")
     return out
+
+
+def split(rowptr, colidx, vals, frac: float, seed: int):
+    """Seeded held-out split of the stored entries: entry k is a test entry iff Philox word
+    (seed, SPLIT_STREAM, k) < frac * 2^32.  Returns (train, test), each a CSR triple
+    (rowptr int64, colidx int32, vals float32) over the same m rows, entries in their original
+    order; the two are disjoint and together hold every entry."""
+    nnz = int(rowptr[-1])
+    if not 0.0 <= frac < 1.0:
+        raise ValueError("frac must lie in [0, 1)")
+    mask = np.empty(nnz, dtype=np.uint8)
+    thr = min(int(round(frac * 2.0 ** 32)), 2 ** 32 - 1)
+    _check(_load().synth_split_mask(seed, SPLIT_STREAM, nnz, thr, _ptr(mask)), "split")
+    test = mask.view(bool)
+    lens = np.diff(rowptr)
+    n_test = np.zeros(len(lens), dtype=np.int64)
+    nonempty = lens > 0
+    if nnz:
+        # per-row sums over [rowptr[u], rowptr[u+1]) (reduceat is wrong on empty rows: masked)
+        n_test[nonempty] = np.add.reduceat(mask, rowptr[:-1][nonempty], dtype=np.int64)
+
+    def csr(counts, sel):
+        ptr = np.zeros(len(rowptr), dtype=np.int64)
+        np.cumsum(counts, out=ptr[1:])
+        return ptr, colidx[sel], vals[sel]
+
+    return csr(lens - n_test, ~test), csr(n_test, test)
 
 
 def transpose(m: int, n: int, rowptr, colidx, vals):

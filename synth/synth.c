@@ -385,6 +385,17 @@ int synth_normal(uint64_t seed, uint32_t stream, int64_t count, double std, floa
     return SYNTH_OK;
 }
 
+/* Held-out split: stored entry k goes to the test set iff the first word of Philox block
+   (k, 0) of the stream is below `threshold` (threshold / 2^32 = the test fraction). */
+int synth_split_mask(uint64_t seed, uint32_t stream, int64_t count, uint32_t threshold,
+                     uint8_t* out) {
+    if (count < 0 || (count > 0 && !out)) return SYNTH_ERR_ARG;
+    skey k = make_key(seed, stream);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) out[i] = draw(k, (uint64_t)i, 0u).v[0] < threshold;
+    return SYNTH_OK;
+}
+
 /* ------------------------------------------------------------------ CSR -> CSC ------- */
 
 /* Stable counting-sort transpose: within each column the row indices stay ascending and
