@@ -59,6 +59,10 @@ def parse():
                          "train/test split, test RMSE per iteration, with and without async "
                          "checkpoints (one JSON line)")
     ap.add_argument("--test-frac", type=float, default=0.01)
+    ap.add_argument("--stream", action="store_true",
+                    help="instead of the step benchmark: half-sweeps with R streamed from pinned "
+                         "host memory in row batches (PCIe-inclusive; one JSON line)")
+    ap.add_argument("--batch-entries", type=int, default=16_000_000)
     ap.add_argument("--checkpoint-every", type=int, default=5)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
@@ -251,6 +255,74 @@ def driver_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def stream_bench(args):
+    """Half-sweeps with each side of R streamed from pinned host memory (row batches)."""
+    import torch
+    import synth
+    from paper_1603_03820_amd import als, driver, stream
+
+    dev = torch.device("cuda", 0)
+    p = synth.config(args.config, f=args.f)
+    csc = p.csc()
+    f = p.f
+    ctx = als.Context(0, max(f, 16))
+    sw_u = stream.StreamedSweep(ctx, stream.HostCSR(p.rowptr, p.colidx, p.vals), p.n, f,
+                                args.batch_entries)
+    sw_i = stream.StreamedSweep(ctx, stream.HostCSR(*csc), p.m, f, args.batch_entries)
+    theta = torch.from_numpy(p.theta0).to(dev)
+    x = torch.empty((p.m, f), dtype=torch.float32, device=dev)
+
+    def step():
+        sw_u.half_sweep(p.lam, theta, x)
+        sw_i.half_sweep(p.lam, x, theta)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    b0 = sw_u.h2d_bytes + sw_i.h2d_bytes
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    h2d = sw_u.h2d_bytes + sw_i.h2d_bytes - b0
+    # reference: one pinned 1 GiB host-to-device copy, and the resident half-sweeps
+    src = torch.empty(1 << 28, dtype=torch.float32).pin_memory()
+    dst = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    copy_gbs = (1 << 30) / (time.perf_counter() - t1) / 1e9
+    del src, dst
+    dp = driver.DeviceProblem.from_host(p.m, p.n, f, p.lam, p.rowptr, p.colidx, p.vals, *csc,
+                                        dev)
+    driver.update_x(ctx, dp, theta, x)
+    driver.update_theta(ctx, dp, x, theta)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        driver.update_x(ctx, dp, theta, x)
+        driver.update_theta(ctx, dp, x, theta)
+    torch.cuda.synchronize()
+    resident = 2.0 * args.steps / (time.perf_counter() - t2)
+    out = {
+        "metric": "ALS half-sweeps/s with R streamed from pinned host memory (PCIe-inclusive)",
+        "value": round(2.0 * args.steps / el, 3), "unit": "half-sweeps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{p.name}: m={p.m} n={p.n} nnz={p.nnz} f={f} lambda={p.lam}",
+                   "batch_entries": args.batch_entries,
+                   "batches": {"user": len(sw_u.batches), "item": len(sw_i.batches)}},
+        "h2d_bytes_per_step": h2d // args.steps,
+        "h2d_gbs_achieved": round(h2d / el / 1e9, 2),
+        "h2d_gbs_pinned_copy": round(copy_gbs, 2),
+        "resident_half_sweeps_per_s": round(resident, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -259,6 +331,9 @@ def main():
         sys.exit(2)
     if args.driver:
         driver_bench(args)
+        return
+    if args.stream:
+        stream_bench(args)
         return
     import torch
     import synth

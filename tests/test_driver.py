@@ -65,3 +65,29 @@ def test_checkpoint_round_trip_host(tmp_path):
     it, x3, th3 = driver.load_checkpoint(str(tmp_path), "cpu", iteration=3)
     assert it == 3 and torch.equal(x3, x) and torch.equal(th3, th)
     assert not list(tmp_path.glob("*.tmp"))
+
+
+@pytest.mark.parametrize("batch", [1, 7, 60, 10**9])
+def test_stream_batches_cover_whole_rows(batch):
+    from paper_1603_03820_amd import stream
+    p = synth.make(500, 80, 20_000, rows="lognormal", zipf=0.9, f=8, model="movie", seed=5)
+    rp = p.rowptr.copy()
+    rp[1:] += 0   # (copy: the plan must not modify its input)
+    b = stream.plan_batches(p.rowptr, batch)
+    assert np.array_equal(rp, p.rowptr)
+    assert b[0][0] == 0 and b[-1][1] == p.m
+    assert all(u1 > u0 for u0, u1 in b) and all(b[i][1] == b[i + 1][0] for i in range(len(b) - 1))
+    for u0, u1 in b:
+        ne = int(p.rowptr[u1] - p.rowptr[u0])
+        assert ne <= batch or u1 == u0 + 1
+        # maximal: the next row would not have fit
+        if u1 < p.m:
+            assert int(p.rowptr[u1 + 1] - p.rowptr[u0]) > batch
+
+
+def test_stream_batches_with_empty_rows():
+    from paper_1603_03820_amd import stream
+    rowptr = np.array([0, 0, 0, 5, 5, 6, 6], dtype=np.int64)
+    b = stream.plan_batches(rowptr, 3)
+    assert b[0][0] == 0 and b[-1][1] == 6
+    assert all(b[i][1] == b[i + 1][0] for i in range(len(b) - 1))
