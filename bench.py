@@ -63,6 +63,9 @@ def parse():
                     help="instead of the step benchmark: half-sweeps with R streamed from pinned "
                          "host memory in row batches (PCIe-inclusive; one JSON line)")
     ap.add_argument("--batch-entries", type=int, default=16_000_000)
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the step benchmark: the half-sweeps under each design "
+                         "alternative (gather form x last-block form), one JSON line")
     ap.add_argument("--checkpoint-every", type=int, default=5)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
@@ -323,6 +326,70 @@ def stream_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def ablation_bench(args):
+    """User and item half-sweeps under each design alternative the library can select: the
+    gather (bounded buffer loads vs 64-bit global loads: the analogue of the paper's texture
+    cache ablation) and the last block column (quad form vs 16x16 tiles)."""
+    import torch
+    import synth
+    from paper_1603_03820_amd import als, driver
+
+    dev = torch.device("cuda", 0)
+    p = synth.config(args.config, f=args.f)
+    csc = p.csc()
+    f = p.f
+    dp = driver.DeviceProblem.from_host(p.m, p.n, f, p.lam, p.rowptr, p.colidx, p.vals, *csc,
+                                        dev)
+    theta0 = torch.from_numpy(p.theta0).to(dev)
+    x = torch.empty((p.m, f), dtype=torch.float32, device=dev)
+    th = torch.empty_like(theta0)
+    variants = [("buffer", "quad"), ("buffer", "tiles"), ("global", "quad"), ("global", "tiles")]
+    rows = []
+    for gather, last in variants:
+        env = {"ALS_GATHER": "global" if gather == "global" else None,
+               "ALS_LAST_BLOCK": "tiles" if last == "tiles" else None}
+        saved = {k: os.environ.get(k) for k in env}
+        for k, v in env.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+        try:
+            ctx = als.Context(0, max(f, 16))
+        finally:
+            for k, v in saved.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
+        for _ in range(args.warmup):
+            driver.update_x(ctx, dp, theta0, x)
+            driver.update_theta(ctx, dp, x, th)
+        torch.cuda.synchronize()
+        als.als_profile_begin(ctx, 2 * args.steps)
+        for _ in range(args.steps):
+            driver.update_x(ctx, dp, theta0, x)
+            driver.update_theta(ctx, dp, x, th)
+        torch.cuda.synchronize()
+        prof = np.array([sum(pr) for pr in als.als_profile_end(ctx, 2 * args.steps)])
+        prof = prof.reshape(-1, 2)
+        rows.append({"gather": gather, "last_block": last,
+                     "user_ms": round(float(np.median(prof[:, 0])), 4),
+                     "item_ms": round(float(np.median(prof[:, 1])), 4)})
+        del ctx
+    base = rows[0]["user_ms"] + rows[0]["item_ms"]
+    for r in rows:
+        r["half_sweep_pair_vs_default"] = round((r["user_ms"] + r["item_ms"]) / base, 4)
+    out = {"metric": "ALS half-sweep time under each kernel design alternative (median ms)",
+           "value": round(2e3 / base, 3), "unit": "half-sweeps/s (default design)", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+           "dtype": "f32", "data": "synthetic",
+           "config": {"workload": f"{p.name}: m={p.m} n={p.n} nnz={p.nnz} f={f} "
+                                  f"lambda={p.lam}"},
+           "variants": rows}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -334,6 +401,9 @@ def main():
         return
     if args.stream:
         stream_bench(args)
+        return
+    if args.ablation:
+        ablation_bench(args)
         return
     import torch
     import synth

@@ -66,7 +66,13 @@ size_t als_workspace_bytes(int device, int32_t f_max);
 
 /* Create a context on `device` using the caller's device workspace (at least
    als_workspace_bytes(device, f_max) bytes, 256-byte aligned; owned by the caller, who keeps
-   it alive until als_destroy).  f_max bounds the f of later calls. */
+   it alive until als_destroy).  f_max bounds the f of later calls.
+   Two environment variables, read here, select design alternatives of the same computation
+   (for tests and ablation; results agree within the parity tolerance):
+     ALS_GATHER=global      gather theta/x with 64-bit global loads at every size (otherwise
+                            bounded buffer loads whenever the factor is below 2 GiB);
+     ALS_LAST_BLOCK=tiles   accumulate the last block column with 16x16x4 tiles even when its
+                            quad form applies (f = 0 or 4 mod 16). */
 int als_init(als_ctx** ctx, int device, void* workspace, size_t workspace_bytes, int32_t f_max);
 
 /* Release the context (not the workspace).  Does not synchronise. */

@@ -59,10 +59,6 @@ constexpr int tu(int nb, int I, int J) { return I * nb - I * (I - 1) / 2 + (J - 
 // floats per partial-accumulator slot: tiles, 4 per lane
 constexpr int slot_floats(int nb) { return ntiles(nb) * 4 * kWave; }
 
-__device__ __forceinline__ float readlane_f(float v, int lane) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
-}
-
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
     return __builtin_bit_cast(
@@ -100,30 +96,6 @@ __device__ __forceinline__ float row_sum16(float v) {
     v += dpp_f<0x141>(v);   // row_half_mirror
     v += dpp_f<0x140>(v);   // row_mirror
     return v;
-}
-
-// Sum over the 16 lanes of a DPP row (lanes 16g..16g+15) of each of four values, returned to all
-// 16 lanes with the same bits: swap neighbours, swap pairs (quad_perm), then mirror within 8 and
-// within 16, each step one v_add with a DPP operand.  The four chains interleave, so each DPP
-// read sits three instructions after the write of its source.
-__device__ __forceinline__ void row_sum16x4(float& v0, float& v1, float& v2, float& v3) {
-#define ALS_ADD4(CTRL)                                                                   \
-    "v_add_f32_dpp %0, %0, %0 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
-    "v_add_f32_dpp %1, %1, %1 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
-    "v_add_f32_dpp %2, %2, %2 " CTRL " row_mask:0xf bank_mask:0xf\n\t"                  \
-    "v_add_f32_dpp %3, %3, %3 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
-    asm volatile("s_nop 1\n\t"
-                 ALS_ADD4("quad_perm:[1,0,3,2]")
-                 ALS_ADD4("quad_perm:[2,3,0,1]")
-                 ALS_ADD4("row_half_mirror")
-                 ALS_ADD4("row_mirror")
-                 : "+v"(v0), "+v"(v1), "+v"(v2), "+v"(v3));
-#undef ALS_ADD4
-}
-__device__ __forceinline__ void row_sum16x4(f4& v) {
-    float a = v[0], b = v[1], c = v[2], d = v[3];
-    row_sum16x4(a, b, c, d);
-    v = f4{a, b, c, d};
 }
 
 // Sums over the 16 lanes of a DPP row of v[0..3], transposed: lane c of the row returns the sum
@@ -1285,6 +1257,7 @@ struct als_ctx {
     int prof_cap;
     int prof_count;
     bool global_gather;    // use the 64-bit-load gather for every size (ALS_GATHER=global)
+    bool tile_last_block;  // 16x16 tiles for the last block column always (ALS_LAST_BLOCK=tiles)
 };
 
 namespace {
@@ -1346,7 +1319,8 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     // the quad form of the last block column: when its theta columns fill whole quads (none or
     // one) and the rating starts a quad of its own
     const int f_last = f - 16 * (NB - 1);
-    const int quads = (f_last == 0 || f_last == 4) ? f_last / 4 + 1 : 0;
+    const int quads =
+        (!ctx->tile_last_block && (f_last == 0 || f_last == 4)) ? f_last / 4 + 1 : 0;
     if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
         if (quads == 1)
             hipLaunchKernelGGL((k_herm_solve<NB, true, 1>), dim3(W), dim3(kWave), 0, st, rowptr,
@@ -1410,6 +1384,8 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
     {
         const char* g = getenv("ALS_GATHER");
         ctx->global_gather = g && strcmp(g, "global") == 0;
+        const char* t = getenv("ALS_LAST_BLOCK");
+        ctx->tile_last_block = t && strcmp(t, "tiles") == 0;
     }
     ctx->nb_max = nb_of(f_max);
     ctx->lay = make_layout(ctx->waves, ctx->nb_max, ctx->cus);

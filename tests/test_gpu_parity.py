@@ -110,6 +110,31 @@ def ctx_global():
         del os.environ["ALS_GATHER"]
 
 
+@pytest.fixture(scope="module")
+def ctx_tiles():
+    """A context that accumulates the last block column with 16x16 tiles even where the quad
+    form applies (the design alternative the quad form replaced)."""
+    import os
+    from paper_1603_03820_amd import als
+    os.environ["ALS_LAST_BLOCK"] = "tiles"
+    try:
+        return als.Context(0, 128)
+    finally:
+        del os.environ["ALS_LAST_BLOCK"]
+
+
+@pytest.mark.parametrize("f", [16, 100, 128])
+def test_tile_form_of_last_block(ctx_tiles, orc, f):
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=779)
+    check_lockstep(ctx_tiles, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"tile-form last block movie-small f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 780, 1.0 / np.sqrt(f))
+    check_lockstep(ctx_tiles, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"tile-form last block movie-small f={f} item")
+
+
 @pytest.mark.parametrize("f", [7, 100, 128])
 def test_global_gather_form(ctx_global, orc, f):
     p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
