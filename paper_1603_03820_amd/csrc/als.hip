@@ -54,6 +54,9 @@ constexpr int kMaxWavesPerCU = 32;
 constexpr int kRmseWavesPerCU = 32;                // RMSE: up to 8 waves per SIMD (occupancy)
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
+// the quad form with a theta quad (f = 16 (NB - 1) + 4) exists for NB whose f is in range
+template <int NB>
+constexpr bool kQuad2 = 16 * (NB - 1) + 4 <= ALS_F_MAX;
 // upper block-triangle, row-major: tile (I, J) with I <= J
 constexpr int tu(int nb, int I, int J) { return I * nb - I * (I - 1) / 2 + (J - I); }
 // floats per partial-accumulator slot: tiles, 4 per lane
@@ -227,33 +230,38 @@ __device__ __forceinline__ void mfma_step(const float (&v)[NB], const float (&w)
 // The quad accumulators into standard tiles acc[tu(NB, I, NB-1)]: the tile's lane (g, c),
 // register r needs M[16 I + 4 g + r][16 (NB-1) + c] = the sum over entry slots e = 0..3, in that
 // order, of q[I][c / 4] at lane 16 e + 4 g + (c & 3), register r, for the theta columns, and of
-// b[I] at lane 16 e + 4 g + r for the rating column; columns past it stay 0.
-// scratch: NB * 64 vectors of LDS.
+// b[I] at lane 16 e + 4 g + r for the rating column; columns past it stay 0.  One LDS exchange
+// for both.  scratch: (P - 1) NB 64 vectors then NB 64 floats, 16-byte aligned.
+template <int NB, int P>
+constexpr int quad_scratch_bytes() {
+    return (P - 1) * NB * kWave * 16 + NB * kWave * 4;
+}
 template <int NB, int P>
 __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc)[ntiles(NB)],
-                                              f4* scratch, int lane) {
+                                              void* scratch, int lane) {
     const int g = lane >> 4, c = lane & 15;
+    f4* sq = reinterpret_cast<f4*>(scratch);
+    float* sb = reinterpret_cast<float*>(sq + (P - 1) * NB * kWave);
+#pragma unroll
+    for (int p = 0; p + 1 < P; ++p)
+#pragma unroll
+        for (int I = 0; I < NB; ++I) sq[(p * NB + I) * kWave + lane] = qa.q[I][p];
+#pragma unroll
+    for (int I = 0; I < NB; ++I) sb[I * kWave + lane] = qa.b[I];
+    __syncthreads();
 #pragma unroll
     for (int I = 0; I < NB; ++I) acc[tu(NB, I, NB - 1)] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int p = 0; p + 1 < P; ++p) {
-#pragma unroll
-        for (int I = 0; I < NB; ++I) scratch[I * kWave + lane] = qa.q[I][p];
-        __syncthreads();
         if ((c >> 2) == p) {
             const int src = 4 * g + (c & 3);
 #pragma unroll
             for (int I = 0; I < NB; ++I) {
-                const f4* s = scratch + I * kWave + src;
+                const f4* s = sq + (p * NB + I) * kWave + src;
                 acc[tu(NB, I, NB - 1)] = ((s[0] + s[16]) + s[32]) + s[48];
             }
         }
-        __syncthreads();
     }
-    float* sb = reinterpret_cast<float*>(scratch);
-#pragma unroll
-    for (int I = 0; I < NB; ++I) sb[I * kWave + lane] = qa.b[I];
-    __syncthreads();
     if (c == 4 * (P - 1)) {
 #pragma unroll
         for (int I = 0; I < NB; ++I) {
@@ -742,10 +750,11 @@ __device__ __forceinline__ f4 back_matvec(int k, const f4 (&acc)[ntiles(NB)],
 // (Block::panel).  The augmented column carries b through the same updates, so its entries
 // become y = L^{-1} b.  Back substitution x_K = W_K^T (y_K - sum_{I>K} D_{K,I} x_I) runs last
 // block first.  Only real pivots (rows < f) are factored; the last block's padding is the
-// identity.  Returns false if a pivot was not positive; writes x_u (f floats) to xrow.
+// identity.  Returns false if a pivot was not positive; leaves the solution in S.x (zero past
+// f).  The same code solves the short-row system of k_short_rows (there f is the row's length).
 template <int NB>
-__device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float lam_n,
-                                          SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
+__device__ __forceinline__ bool solve_core(f4 (&acc)[ntiles(NB)], int f, float lam_n,
+                                           SolveLds<NB>& S, int lane) {
     const int g = lane >> 4, c = lane & 15;
     const int nlast = f - 16 * (NB - 1);   // real columns of the last block; b is its column nlast
     // -M: the factorisation below keeps unfactored tiles negated (the regularisation joins each
@@ -786,6 +795,14 @@ __device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float la
         if (c < 4) S.x[16 * K + kq] = real ? xv : 0.f;
         __syncthreads();
     }
+    return ok;
+}
+
+// solve_core, then x_u (f floats, NaN if a pivot was not positive) to xrow.
+template <int NB>
+__device__ __forceinline__ bool solve_row(f4 (&acc)[ntiles(NB)], int f, float lam_n,
+                                          SolveLds<NB>& S, float* __restrict__ xrow, int lane) {
+    const bool ok = solve_core<NB>(acc, f, lam_n, S, lane);
     for (int j = lane; j < f; j += kWave) xrow[j] = ok ? S.x[j] : __builtin_nanf("");
     return ok;
 }
@@ -895,7 +912,11 @@ void k_herm_solve(
             }
             gram_loop<NB, P>(gat, colidx, vals, cur.beg, cur.end, acc, qa, ring, lane, in);
             if (more) gram_stage(gat, ix, ring, lane, in);
-            if constexpr (P > 0) quad_to_tiles<NB, P>(qa, acc, reinterpret_cast<f4*>(lds.W), lane);
+            if constexpr (P > 0) {
+                static_assert(quad_scratch_bytes<NB, P>() <= sizeof(SolveLds<NB>),
+                              "the quad exchange reuses the solve's LDS");
+                quad_to_tiles<NB, P>(qa, acc, &lds, lane);
+            }
             // the solve is a latency-bound chain; raised priority lets it win issue slots over
             // the other wave's independent Gram MFMAs, which then fill the solve's gaps
             __builtin_amdgcn_s_setprio(2);
@@ -1172,9 +1193,11 @@ int occupancy_waves(int cus, int* waves) {
     int blocks = 1 << 30;
     const void* forms[] = {(const void*)k_herm_solve<NB, true, 0>,
                            (const void*)k_herm_solve<NB, true, 1>,
-                           (const void*)k_herm_solve<NB, true, 2>,
+                           kQuad2<NB> ? (const void*)k_herm_solve<NB, true, kQuad2<NB> ? 2 : 1>
+                                      : nullptr,
                            (const void*)k_herm_solve<NB, false, 0>};
     for (const void* k : forms) {
+        if (!k) continue;
         int b = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, kWave, 0) != hipSuccess) return -1;
         if (b < blocks) blocks = b;
@@ -1326,10 +1349,12 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
             hipLaunchKernelGGL((k_herm_solve<NB, true, 1>), dim3(W), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
                                chunk_ctr);
-        else if (quads == 2)
-            hipLaunchKernelGGL((k_herm_solve<NB, true, 2>), dim3(W), dim3(kWave), 0, st, rowptr,
-                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
-                               chunk_ctr);
+        else if (quads == 2) {
+            if constexpr (kQuad2<NB>)
+                hipLaunchKernelGGL((k_herm_solve<NB, true, 2>), dim3(W), dim3(kWave), 0, st,
+                                   rowptr, colidx, vals, theta, m, n, f, lambda, C, bounds, x,
+                                   slots, nonspd, chunk_ctr);
+        }
         else
             hipLaunchKernelGGL((k_herm_solve<NB, true, 0>), dim3(W), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
