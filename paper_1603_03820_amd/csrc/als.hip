@@ -456,7 +456,9 @@ __device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* rin
 // gram_stage left in the ring and in `in`.  Per step the body takes the step's operands
 // (body.take(B, r, ok): B the loaded values, r the rating, ok whether the step's entry lies in the
 // piece), then -- after the gather kDepth steps ahead has been issued -- runs the step
-// (body.run<J>(), J the step's place in its group of kGroup; the loop always runs whole groups).
+// (body.run<J>(), J the step's place in its group of kGroup; the loop always runs whole groups:
+// stopping inside the last group costs more, as a branch per step or as a second copy of the
+// group, than the steps of zeros it would skip).
 // ring: this wave's LDS ring of kRing entries.  Returns with the ring idle.
 template <class G, class Body>
 __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restrict__ colidx,
@@ -538,7 +540,7 @@ struct FactorRegs {
 // Pivot kk = 4 B + P of factor_tile.  The next pivot waits on this one's readlane, s, s^2, the
 // product for the next row and that row's update, so the next row (P + 1) is updated first.
 // One transcendental per pivot (s = piv^{-1/2}; 1/piv = s^2).
-template <int B, int P>
+template <int B, int P, bool kFull>
 __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin, int& pmax,
                                              float* ystore) {
     constexpr int kk = 4 * B + P;
@@ -559,20 +561,25 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
     // sits at least n - 1 instructions after the previous pivot's write of it (n row updates
     // here); a block's first pivot always waits (its sources were loaded or carried over the
     // block's branch).
+    // (without the later rows, kFull = false, every pivot waits)
     constexpr int n = (3 - P) + (3 - B);
-    if constexpr (P == 0 || n < 3) dpp_settle();
+    if constexpr (P == 0 || n < 3 || !kFull) dpp_settle();
     if constexpr (P < 3) {
         R.wr[P + 1] = fmac_bcast<kk>(R.wr[P + 1], R.tr[P + 1], aw);
         R.tr[P + 1] = fmac_bcast<kk>(R.tr[P + 1], R.tr[P + 1], at);
     }
 #pragma unroll
     for (int j = P + 2; j < 4; ++j) R.wr[j] = fmac_bcast<kk>(R.wr[j], R.tr[j], aw);
+    if constexpr (kFull) {
 #pragma unroll
-    for (int bb = B + 1; bb < 4; ++bb) R.wo[bb] = fmac_bcast<kk>(R.wo[bb], R.to[bb], aw);
+        for (int bb = B + 1; bb < 4; ++bb) R.wo[bb] = fmac_bcast<kk>(R.wo[bb], R.to[bb], aw);
+    }
 #pragma unroll
     for (int j = P + 2; j < 4; ++j) R.tr[j] = fmac_bcast<kk>(R.tr[j], R.tr[j], at);
+    if constexpr (kFull) {
 #pragma unroll
-    for (int bb = B + 1; bb < 4; ++bb) R.to[bb] = fmac_bcast<kk>(R.to[bb], R.to[bb], at);
+        for (int bb = B + 1; bb < 4; ++bb) R.to[bb] = fmac_bcast<kk>(R.to[bb], R.to[bb], at);
+    }
 }
 
 // Factor and invert the symmetric 16 x 16 diagonal tile T, staged negated in S.T (row-major:
@@ -594,15 +601,25 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
 // inside a block).  In the last block the row nlast is the augmented b row, whose L entries are y
 // (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot was positive (and not
 // NaN) iff pmin > 0 and pmax <= the bits of +inf.
-template <int NB, int B = 0>
+// kFull = false: the tile has at most 4 real rows (the last block when f - 16 (NB - 1) <= 4).
+// Then the rows past the first block are neither pivots nor needed (the b row's L entries come
+// from the pivot rows' column nlast), so only block 0 is factored and rows 4..15 of -W are
+// written as zeros (the back substitution multiplies them by zeros).
+template <int NB, bool kFull, int B = 0>
 __device__ __forceinline__ void factor_blocks(SolveLds<NB>& S, FactorRegs& R, int K, int npiv,
                                               float* ystore, int& pmin, int& pmax, int lane) {
     const int g = lane >> 4, c = lane & 15;
     if (4 * B < npiv) {
-        factor_pivot<B, 0>(R, 4 * B + 0 < npiv, pmin, pmax, ystore);
-        factor_pivot<B, 1>(R, 4 * B + 1 < npiv, pmin, pmax, ystore);
-        factor_pivot<B, 2>(R, 4 * B + 2 < npiv, pmin, pmax, ystore);
-        factor_pivot<B, 3>(R, 4 * B + 3 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 0, kFull>(R, 4 * B + 0 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 1, kFull>(R, 4 * B + 1 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 2, kFull>(R, 4 * B + 2 < npiv, pmin, pmax, ystore);
+        factor_pivot<B, 3, kFull>(R, 4 * B + 3 < npiv, pmin, pmax, ystore);
+    }
+    if constexpr (!kFull) {
+        const f4 z = f4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * g]) =
+            g == 0 ? f4{R.wr[0], R.wr[1], R.wr[2], R.wr[3]} : z;
+        return;
     }
     if (g == 0)
         *reinterpret_cast<f4*>(&S.W[K][c * 16 + 4 * B]) = f4{R.wr[0], R.wr[1], R.wr[2], R.wr[3]};
@@ -617,28 +634,33 @@ __device__ __forceinline__ void factor_blocks(SolveLds<NB>& S, FactorRegs& R, in
         const f4 u1 = *reinterpret_cast<const f4*>(&X[c * 8 + 4]);
         R.tr[0] = u0[0]; R.wr[0] = u0[1]; R.tr[1] = u0[2]; R.wr[1] = u0[3];
         R.tr[2] = u1[0]; R.wr[2] = u1[1]; R.tr[3] = u1[2]; R.wr[3] = u1[3];
-        factor_blocks<NB, B + 1>(S, R, K, npiv, ystore, pmin, pmax, lane);
+        factor_blocks<NB, kFull, B + 1>(S, R, K, npiv, ystore, pmin, pmax, lane);
     }
 }
 
-template <int NB>
+template <int NB, bool kFull>
 __device__ __forceinline__ void factor_tile(SolveLds<NB>& S, int K, int npiv, int nlast,
                                             int& pmin, int& pmax, int lane) {
     const int g = lane >> 4, c = lane & 15;
     FactorRegs R;
 #pragma unroll
     for (int j = 0; j < 4; ++j) R.tr[j] = S.T[c * 16 + j];
-#pragma unroll
-    for (int bb = 1; bb < 4; ++bb) R.to[bb] = S.T[c * 16 + 4 * bb + g];
     // -identity: row j in lanes c == j; row 4b' + g in lanes 16 g + 4 b' + g
 #pragma unroll
     for (int j = 0; j < 4; ++j) R.wr[j] = lane_select_minus_one(0x0001000100010001ull << j);
-#pragma unroll
-    for (int bb = 1; bb < 4; ++bb)
-        R.wo[bb] = lane_select_minus_one(0x0008000400020001ull << (4 * bb));
     R.to[0] = R.wo[0] = 0.f;
+    if constexpr (kFull) {
+#pragma unroll
+        for (int bb = 1; bb < 4; ++bb) R.to[bb] = S.T[c * 16 + 4 * bb + g];
+#pragma unroll
+        for (int bb = 1; bb < 4; ++bb)
+            R.wo[bb] = lane_select_minus_one(0x0008000400020001ull << (4 * bb));
+    } else {
+#pragma unroll
+        for (int bb = 1; bb < 4; ++bb) R.to[bb] = R.wo[bb] = 0.f;
+    }
     float* ystore = ((K == NB - 1) && lane == nlast) ? &S.y[16 * K] : nullptr;
-    factor_blocks<NB>(S, R, K, npiv, ystore, pmin, pmax, lane);
+    factor_blocks<NB, kFull>(S, R, K, npiv, ystore, pmin, pmax, lane);
 }
 
 // Block K's acc-indexed steps, one instantiation per K (the block loop runs at run time so the
@@ -751,7 +773,7 @@ __device__ __forceinline__ f4 back_matvec(int k, const f4 (&acc)[ntiles(NB)],
 // become y = L^{-1} b.  Back substitution x_K = W_K^T (y_K - sum_{I>K} D_{K,I} x_I) runs last
 // block first.  Only real pivots (rows < f) are factored; the last block's padding is the
 // identity.  Returns false if a pivot was not positive; leaves the solution in S.x (zero past
-// f).  The same code solves the short-row system of k_short_rows (there f is the row's length).
+// f).
 template <int NB>
 __device__ __forceinline__ bool solve_core(f4 (&acc)[ntiles(NB)], int f, float lam_n,
                                            SolveLds<NB>& S, int lane) {
@@ -769,7 +791,10 @@ __device__ __forceinline__ bool solve_core(f4 (&acc)[ntiles(NB)], int f, float l
     for (int K = 0; K < NB; ++K) {
         stage_diag<NB>(K, acc, S, lam_n, nlast, lane);
         __syncthreads();
-        factor_tile<NB>(S, K, (K < NB - 1) ? 16 : nlast, nlast, pmin, pmax, lane);
+        if (K == NB - 1 && nlast <= 4)
+            factor_tile<NB, false>(S, K, nlast, nlast, pmin, pmax, lane);
+        else
+            factor_tile<NB, true>(S, K, (K < NB - 1) ? 16 : nlast, nlast, pmin, pmax, lane);
         __syncthreads();
         panel_update<NB>(K, acc, S, nlast, lane);
     }
