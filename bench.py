@@ -155,6 +155,27 @@ def measure_peaks(dev):
             "note": "unpacked FP32 FMA (packed FP32 is not used); copy = read + write bytes"}
 
 
+def csc_build(ctx, dp, p, reps=3):
+    """The item side's input, R^T as CSC, built on the device by als_csr_to_csc from the resident
+    CSR (outside the timed steps): median HIP-event time, and whether it equals, bit for bit, the
+    CSC the host-side input generator produced (which the timed steps read)."""
+    import torch
+    from paper_1603_03820_amd import als
+    out = (torch.empty_like(dp.colptr), torch.empty_like(dp.rowidx), torch.empty_like(dp.vals_t))
+    ts = []
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        als.als_csr_to_csc(ctx, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, nnz=p.nnz, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    same = (torch.equal(out[0], dp.colptr) and torch.equal(out[1], dp.rowidx)
+            and torch.equal(out[2].view(torch.int32), dp.vals_t.view(torch.int32)))
+    return {"ms": round(float(np.median(ts[1:])), 3), "matches_generator_csc": bool(same),
+            "note": "R^T on the device (als_csr_to_csc), not part of a step"}
+
+
 def cpu_baseline(p, csc, budget, stride=0):
     """The fp64 oracle as it stands, on every k-th row of each side (k chosen so the sample has
     about `budget` algorithmic flops, or `stride`), extrapolated to a full half-sweep pair by
@@ -523,6 +544,7 @@ def main():
         "roofline": roofline,
         "gen_s": round(t_gen, 1),
     }
+    out["csc_build"] = csc_build(ctx, dp, p)
     if not args.no_peaks:
         out["peaks_measured"] = measure_peaks(dev)
         roofline["frac_of_measured_mfma"] = round(

@@ -142,6 +142,27 @@ int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t*
 int als_profile_begin(als_ctx* ctx, int32_t capacity);
 int als_profile_end(als_ctx* ctx, float* ms_out, int32_t capacity, int32_t* count_out);
 
+/*
+ * The transpose R -> R^T as CSC (equivalently the CSR of R^T): the input of the update-Theta
+ * half-sweep, which applies eq. 2 to the columns of R (eq. 3).  Stable: the entries of a column
+ * appear in ascending row order (for a valid CSR, the order of their positions in colidx),
+ * with their ratings carried along, so the result is unique and the same on every run.
+ *   rowptr, colidx, vals : CSR of the m x n matrix (see conventions); m <= INT32_MAX
+ *   colptr               : DEVICE int64[n+1], written: colptr[0] = 0, colptr[n] = nnz
+ *   rowidx, vals_t       : DEVICE int32[nnz], fp32[nnz], written: the row index and rating of
+ *                          each entry, column by column
+ * colidx, vals, rowidx and vals_t must not be null when m > 0 and n > 0 (ALS_ERR_INVALID_ARG).
+ * Outputs must not overlap the inputs.  Scratch is the context's workspace (past its status
+ * block): it holds one int32 counter per column for each of R row blocks, with R chosen to fit
+ * (at most 8 per compute unit, at least 1); if even one block does not fit (about 4 n bytes),
+ * ALS_ERR_WORKSPACE.  Entries with a column outside [0, n) are skipped (not validated otherwise;
+ * colptr[n] then counts only the others).  Queued on `stream`; it shares the workspace with the
+ * other calls of the context, so it must not overlap them in time.
+ */
+int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
+                   int64_t m, int64_t n, int64_t* colptr, int32_t* rowidx, float* vals_t,
+                   void* stream);
+
 /* HIP error code of the most recent ALS_ERR_HIP on this context (0 if none). */
 int als_last_hip_error(const als_ctx* ctx);
 

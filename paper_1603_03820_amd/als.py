@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libals.so")
 ALS_OK = 0
 ALS_F_MAX = 128
 EXPORTED = ("als_workspace_bytes", "als_init", "als_destroy", "als_half_sweep", "als_rmse",
-            "als_status", "als_plan", "als_profile_begin", "als_profile_end",
+            "als_status", "als_plan", "als_csr_to_csc", "als_profile_begin", "als_profile_end",
             "als_last_hip_error", "als_strerror")
 
 
@@ -45,13 +45,14 @@ def _load():
     lib.als_rmse.argtypes = [P, P, P, P, i64, i64, i32, P, P, P, P]
     lib.als_status.argtypes = [P, P, ctypes.POINTER(i64)]
     lib.als_plan.argtypes = [P, P, i64, i32, P, i64, P, P]
+    lib.als_csr_to_csc.argtypes = [P, P, P, P, i64, i64, P, P, P, P]
     lib.als_profile_begin.argtypes = [P, i32]
     lib.als_profile_end.argtypes = [P, P, i32, ctypes.POINTER(i32)]
     lib.als_last_hip_error.argtypes = [P]
     lib.als_strerror.argtypes = [ctypes.c_int]
     lib.als_strerror.restype = ctypes.c_char_p
     for fn in ("als_init", "als_destroy", "als_half_sweep", "als_rmse", "als_status", "als_plan",
-               "als_profile_begin", "als_profile_end", "als_last_hip_error"):
+               "als_csr_to_csc", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
         getattr(lib, fn).restype = ctypes.c_int
     return lib
 
@@ -175,6 +176,30 @@ def als_plan(ctx: Context, rowptr, m: int, f: int, stream=None):
                        _stream(ctx.device, stream))
     _check("als_plan", rc, ctx.handle)
     return bounds, tuple(int(v) for v in params)
+
+
+def als_csr_to_csc(ctx: Context, rowptr, colidx, vals, m: int, n: int, nnz: int | None = None,
+                   out=None, stream=None):
+    """The CSC of the m x n CSR matrix (stable: rows ascending within each column), as device
+    tensors (colptr int64 [n+1], rowidx int32 [nnz], vals_t float32 [nnz]).  nnz defaults to
+    rowptr[m] (read from the device); `out` may supply the three output tensors."""
+    if nnz is None:
+        nnz = int(rowptr[m].item()) if m > 0 else 0
+    if out is None:
+        # at least one element each (an empty tensor's data pointer is null)
+        out = (torch.empty(n + 1, dtype=torch.int64, device=ctx.device),
+               torch.empty(max(nnz, 1), dtype=torch.int32, device=ctx.device),
+               torch.empty(max(nnz, 1), dtype=torch.float32, device=ctx.device))
+    colptr, rowidx, vals_t = out
+    rc = _lib.als_csr_to_csc(ctx.handle, _dev(rowptr, torch.int64, "rowptr", m + 1),
+                             _dev(colidx, torch.int32, "colidx", nnz),
+                             _dev(vals, torch.float32, "vals", nnz), m, n,
+                             _dev(colptr, torch.int64, "colptr", n + 1),
+                             _dev(rowidx, torch.int32, "rowidx", nnz),
+                             _dev(vals_t, torch.float32, "vals_t", nnz),
+                             _stream(ctx.device, stream))
+    _check("als_csr_to_csc", rc, ctx.handle)
+    return colptr, rowidx[:nnz], vals_t[:nnz]
 
 
 def als_profile_begin(ctx: Context, capacity: int):

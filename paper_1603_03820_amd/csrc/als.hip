@@ -34,6 +34,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <climits>
 #include <cstring>
 #include <new>
 
@@ -52,6 +53,7 @@ constexpr int kSmallPerWave = 4;                // small chunks per wave
 constexpr int chunks_of(int waves) { return waves * (1 + kSmallPerWave); }
 constexpr int kMaxWavesPerCU = 32;
 constexpr int kRmseWavesPerCU = 32;                // RMSE: up to 8 waves per SIMD (occupancy)
+constexpr int kTransposeWavesPerCU = 8;            // CSR -> CSC: row blocks per CU (at most)
 
 constexpr int ntiles(int nb) { return nb * (nb + 1) / 2; }
 // the quad form with a theta quad (f = 16 (NB - 1) + 4) exists for NB whose f is in range
@@ -1182,6 +1184,167 @@ __global__ __launch_bounds__(kWave) void k_rmse_final(const int64_t* __restrict_
 
 __global__ void k_reset_counter(unsigned long long* p) { *p = 0ull; }
 
+// ------------------------------------------------------------------ CSR -> CSC -----------
+
+// The transpose R -> R^T that the update-Theta half-sweep reads (eq. 3 is the same method on
+// the columns of R).  Stable: within a column the entries keep the order of their rows.
+// The rows are cut into R row blocks of about nnz / R entries each (whole rows; block b holds
+// rows [tr_row_begin(b), tr_row_begin(b+1))).  cnt[b][v] counts block b's entries in column v;
+// a prefix over b turns it into the offset of block b's first entry within column v, and one
+// wave per block then walks its rows in order, so every column receives its rows ascending.
+// Entries whose column lies outside [0, n) are skipped by every pass (the contract leaves them
+// undefined; skipping keeps every access in bounds).
+
+// First row of row block b: the smallest u with rowptr[u] >= floor(b nnz / R) (binary search).
+__device__ __forceinline__ int64_t tr_row_begin(const int64_t* __restrict__ rowptr, int64_t m,
+                                                int R, int b) {
+    const int64_t nnz = rowptr[m];
+    // floor(nnz b / R) without overflow: nnz = q R + r, r b < R^2
+    const int64_t target = (nnz / R) * b + ((nnz % R) * b) / R;
+    int64_t lo = 0, hi = m;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (rowptr[mid] < target) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void k_tr_zero(int32_t* __restrict__ p, int64_t count) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * 256)
+        p[i] = 0;
+}
+
+// cnt[b][v] += 1 for every entry of row block b (one workgroup per block; the order of the
+// increments does not matter).
+__global__ __launch_bounds__(256) void k_tr_count(const int64_t* __restrict__ rowptr,
+                                                  const int32_t* __restrict__ colidx, int64_t m,
+                                                  int64_t n, int R, int32_t* __restrict__ cnt) {
+    const int b = blockIdx.x;
+    const int64_t k0 = rowptr[tr_row_begin(rowptr, m, R, b)];
+    const int64_t k1 = rowptr[tr_row_begin(rowptr, m, R, b + 1)];
+    int32_t* row = cnt + (size_t)b * (size_t)n;
+    for (int64_t k = k0 + threadIdx.x; k < k1; k += 256) {
+        const int32_t v = colidx[k];
+        if (v >= 0 && v < n) atomicAdd(&row[v], 1);
+    }
+}
+
+// Per column v (one thread each): cnt[b][v] <- the sum over b' < b, and colptr[v] <- the
+// column's total (scanned over v afterwards).
+__global__ __launch_bounds__(256) void k_tr_colscan(int64_t n, int R, int32_t* __restrict__ cnt,
+                                                    int64_t* __restrict__ colptr) {
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (v >= n) return;
+    int32_t run = 0;
+    for (int b = 0; b < R; ++b) {
+        int32_t* c = cnt + (size_t)b * (size_t)n + v;
+        const int32_t t = *c;
+        *c = run;
+        run += t;
+    }
+    colptr[v] = run;
+}
+
+// Exclusive scan of a[0, len) in place, a[len] <- the total: tile sums (kScanTile elements per
+// workgroup), a scan of the tile sums by one workgroup, then each tile scanned with its offset.
+constexpr int kScanPer = 16;
+constexpr int kScanTile = 256 * kScanPer;
+
+// Exclusive scan of one value per thread over a workgroup of 256 (4 waves); returns the prefix
+// and sets *total.
+__device__ __forceinline__ int64_t block_exclusive_scan(int64_t x, int64_t* sh, int64_t* total) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    int64_t inc = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) sh[w] = inc;
+    __syncthreads();
+    int64_t base = 0;
+    for (int i = 0; i < w; ++i) base += sh[i];
+    *total = sh[0] + sh[1] + sh[2] + sh[3];
+    __syncthreads();
+    return base + inc - x;
+}
+
+__global__ __launch_bounds__(256) void k_scan_sums(const int64_t* __restrict__ a, int64_t len,
+                                                   int64_t* __restrict__ sums) {
+    __shared__ int64_t sh[4];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    int64_t x = 0;
+    for (int j = 0; j < kScanPer; ++j) {
+        const int64_t i = base + (int64_t)threadIdx.x * kScanPer + j;
+        if (i < len) x += a[i];
+    }
+    int64_t total;
+    (void)block_exclusive_scan(x, sh, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(256) void k_scan_top(int64_t* __restrict__ sums, int64_t tiles,
+                                                  int64_t* __restrict__ a, int64_t len) {
+    __shared__ int64_t sh[4];
+    int64_t carry = 0;
+    for (int64_t c = 0; c < tiles; c += 256) {
+        const int64_t i = c + threadIdx.x;
+        const int64_t x = i < tiles ? sums[i] : 0;
+        int64_t total;
+        const int64_t ex = block_exclusive_scan(x, sh, &total);
+        if (i < tiles) sums[i] = carry + ex;
+        carry += total;
+    }
+    if (threadIdx.x == 0) a[len] = carry;
+}
+
+__global__ __launch_bounds__(256) void k_scan_apply(int64_t* __restrict__ a, int64_t len,
+                                                    const int64_t* __restrict__ sums) {
+    __shared__ int64_t sh[4];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPer;
+    int64_t v[kScanPer];
+    int64_t x = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        v[j] = base + j < len ? a[base + j] : 0;
+        x += v[j];
+    }
+    int64_t total;
+    int64_t run = sums[blockIdx.x] + block_exclusive_scan(x, sh, &total);
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        if (base + j < len) a[base + j] = run;
+        run += v[j];
+    }
+}
+
+// One wave per row block, its rows in order: each entry goes to colptr[v] + cnt[b][v], which
+// then moves on by one.  The columns of one row are distinct, so the lanes of a row never share
+// a counter; the fence after each row orders its counter updates before the next row's.
+__global__ __launch_bounds__(kWave) void k_tr_scatter(
+    const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    const float* __restrict__ vals, int64_t m, int64_t n, int R, int32_t* __restrict__ cnt,
+    const int64_t* __restrict__ colptr, int32_t* __restrict__ rowidx,
+    float* __restrict__ vals_t) {
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int64_t u0 = tr_row_begin(rowptr, m, R, b), u1 = tr_row_begin(rowptr, m, R, b + 1);
+    int32_t* row = cnt + (size_t)b * (size_t)n;
+    for (int64_t u = u0; u < u1; ++u) {
+        const int64_t k1 = rowptr[u + 1];
+        for (int64_t k = rowptr[u] + lane; k < k1; k += kWave) {
+            const int32_t v = colidx[k];
+            if (v >= 0 && v < n) {
+                const int32_t at = atomicAdd(&row[v], 1);
+                const int64_t pos = colptr[v] + at;
+                rowidx[pos] = (int32_t)u;
+                vals_t[pos] = vals[k];
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    }
+}
+
 // --------------------------------------------------------------------- host side ---------
 
 struct Layout {
@@ -1621,6 +1784,53 @@ int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t*
     hipLaunchKernelGGL(k_plan, dim3((C + 1 + 63) / 64), dim3(64), 0, (hipStream_t)stream, rowptr,
                        m, W, C, (int64_t)kCostPerEntry, row_cost(f), (int64_t)kSnap, bounds_out,
                        nullptr);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
+}
+
+int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
+                   int64_t m, int64_t n, int64_t* colptr, int32_t* rowidx, float* vals_t,
+                   void* stream) {
+    if (!ctx || !rowptr || !colptr || m < 0 || n < 0 || m > INT32_MAX) return ALS_ERR_INVALID_ARG;
+    if (m > 0 && n > 0 && (!colidx || !vals || !rowidx || !vals_t)) return ALS_ERR_INVALID_ARG;
+    if (!aligned(rowptr, 8) || !aligned(colptr, 8) || !aligned(colidx, 4) || !aligned(vals, 4) ||
+        !aligned(rowidx, 4) || !aligned(vals_t, 4))
+        return ALS_ERR_ALIGN;
+    // scratch: everything past the status block (no half-sweep runs meanwhile on this context)
+    const size_t tiles = (size_t)(n + kScanTile - 1) / kScanTile;
+    const size_t sums_bytes = align256(sizeof(int64_t) * (tiles + 1));
+    const size_t avail = ctx->ws_bytes - ctx->lay.bounds;
+    if (avail < sums_bytes + sizeof(int32_t) * (size_t)(n > 0 ? n : 1)) return ALS_ERR_WORKSPACE;
+    int64_t R = n > 0 ? (int64_t)((avail - sums_bytes) / (sizeof(int32_t) * (size_t)n)) : 1;
+    const int64_t r_cap = (int64_t)ctx->cus * kTransposeWavesPerCU;
+    if (R > r_cap) R = r_cap;
+    if (R > m) R = m;
+    if (R < 1) R = 1;
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return ALS_ERR_DEVICE;
+    hipStream_t st = (hipStream_t)stream;
+    int64_t* sums = (int64_t*)(ctx->ws + ctx->lay.bounds);
+    int32_t* cnt = (int32_t*)(ctx->ws + ctx->lay.bounds + sums_bytes);
+    const int64_t cells = R * n;
+    if (cells > 0) {
+        const int64_t zb = (cells + 255) / 256;
+        hipLaunchKernelGGL(k_tr_zero, dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, st,
+                           cnt, cells);
+    }
+    if (m > 0 && n > 0)
+        hipLaunchKernelGGL(k_tr_count, dim3((unsigned)R), dim3(256), 0, st, rowptr, colidx, m, n,
+                           (int)R, cnt);
+    if (n > 0)
+        hipLaunchKernelGGL(k_tr_colscan, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, n,
+                           (int)R, cnt, colptr);
+    if (n > 0)
+        hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)tiles), dim3(256), 0, st, colptr, n, sums);
+    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, sums, (int64_t)tiles, colptr, n);
+    if (n > 0)
+        hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)tiles), dim3(256), 0, st, colptr, n, sums);
+    if (m > 0 && n > 0)
+        hipLaunchKernelGGL(k_tr_scatter, dim3((unsigned)R), dim3(kWave), 0, st, rowptr, colidx,
+                           vals, m, n, (int)R, cnt, colptr, rowidx, vals_t);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
 }
