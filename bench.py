@@ -5,7 +5,9 @@ One step = one ALS iteration on the movie-shaped workload (480,000 x 17,770, 100
 ratings, f = 100, lambda = 0.05): update-X (half-sweep on the CSR), update-Theta (half-sweep
 on the CSC) and the training RMSE, all through the C ABI of include/als.h.  Inputs are
 resident in HBM before the timed region.  `value` = half-sweeps per second over the K timed
-steps (2 per step).
+steps (2 per step).  Step k's RMSE (it reads X_k and Theta_k) runs on a second stream, one wave
+per SIMD, beside step k+1's update-X (which only reads Theta_k; X is double-buffered), and
+step k+1's update-Theta waits for it; --serial-rmse runs it after update-Theta instead.
 
 After the timed region: peak microbenchmarks (FP32 MFMA and VALU FMA rates, an HBM copy) for
 measured denominators, then the fp64 CPU oracle on a bounded row sample (all host threads, plus
@@ -67,6 +69,10 @@ def parse():
                     help="instead of the step benchmark: the half-sweeps under each design "
                          "alternative (gather form x last-block form), one JSON line")
     ap.add_argument("--checkpoint-every", type=int, default=5)
+    ap.add_argument("--serial-rmse", action="store_true",
+                    help="run each step's RMSE after its update-Theta on the same stream (default: "
+                         "on a second stream and context, one wave per SIMD, beside the next "
+                         "step's update-X, with X double-buffered)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
                          "calibration), then one user and one item half-sweep; no JSON")
@@ -457,10 +463,37 @@ def main():
         print("pmc pass done", flush=True)
         return
 
-    def step():
-        driver.update_x(ctx, dp, theta, x)
-        driver.update_theta(ctx, dp, x, theta)
-        als.als_rmse(ctx, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, x, theta, rmse)
+    if not args.serial_rmse:
+        # step k: X_k <- update-X(Theta_{k-1}) into xs[k % 2]; Theta_k <- update-Theta(X_k), once
+        # RMSE_{k-1} (which reads Theta_{k-1}) is done; then RMSE_k(X_k, Theta_k) on the side
+        # stream, where it overlaps update-X of step k+1 (which only reads Theta_k)
+        ctx_r = als.Context(0, max(f, 16))
+        als.als_rmse_waves(ctx_r, 1)
+        main_s = torch.cuda.current_stream(dev)
+        side_s = torch.cuda.Stream(dev)
+        xs = [x, torch.empty_like(x)]
+        theta_ready = [torch.cuda.Event(), torch.cuda.Event()]
+        rmse_done = [torch.cuda.Event(), torch.cuda.Event()]
+        k_box = [0]
+
+        def step():
+            k = k_box[0]
+            xk = xs[k % 2]
+            driver.update_x(ctx, dp, theta, xk)
+            if k > 0:
+                main_s.wait_event(rmse_done[(k - 1) % 2])
+            driver.update_theta(ctx, dp, xk, theta)
+            theta_ready[k % 2].record(main_s)
+            side_s.wait_event(theta_ready[k % 2])
+            als.als_rmse(ctx_r, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, xk, theta, rmse,
+                         stream=side_s)
+            rmse_done[k % 2].record(side_s)
+            k_box[0] = k + 1
+    else:
+        def step():
+            driver.update_x(ctx, dp, theta, x)
+            driver.update_theta(ctx, dp, x, theta)
+            als.als_rmse(ctx, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, x, theta, rmse)
 
     for _ in range(args.warmup):
         step()
@@ -523,7 +556,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{p.name}: m={p.m} n={p.n} nnz={nnz} f={f} lambda={p.lam}",
                    "m": p.m, "n": p.n, "nnz": nnz, "f": f, "lambda": p.lam,
-                   "step": "update-X + update-Theta + training RMSE",
+                   "step": "update-X + update-Theta + training RMSE" + (
+                       " (each RMSE on a second stream, beside the next update-X)"
+                       if not args.serial_rmse else ""),
                    "recipe": {k: v for k, v in p.recipe.items() if k not in ("m", "n", "nnz")}},
         "gflops": round(gflops, 1),
         "pct_fp32_peak": round(100.0 * gflops / 1e3 / FP32_PEAK_TFLOPS, 2),

@@ -100,12 +100,20 @@ int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
  * Training root-mean-square error over the stored entries (the evaluation metric of the
  * paper's experiments, on the training set):
  *   *rmse_out = sqrt( sum over stored (u,v) of (r_uv - x_u . theta_v)^2 / nnz )
- * Residuals in fp32, sums in fp64 in a fixed order.  rmse_out is a DEVICE double; 0 when
- * nnz = 0.
+ * Residuals in fp32, sums in fp64 in a fixed order (per chunk of entries, then over the
+ * chunks).  rmse_out is a DEVICE double; 0 when nnz = 0.
  */
 int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
              int64_t m, int64_t n, int32_t f, const float* x, const float* theta,
              double* rmse_out, void* stream);
+
+/* Width of later als_rmse calls on this context: at most `waves_per_simd` resident waves per
+   SIMD (1..8), or as many as fit (0, the default).  The entries are always cut into the same
+   fixed chunks, claimed by the running waves in order, and summed per chunk in a fixed order,
+   so the result does not depend on the width.  A narrow RMSE can run beside a half-sweep of
+   another context (its own workspace) on another stream: at f <= 112 the half-sweep leaves
+   room for one RMSE wave per SIMD.  ALS_ERR_INVALID_ARG outside 0..8. */
+int als_rmse_waves(als_ctx* ctx, int32_t waves_per_simd);
 
 /* Synchronise `stream`, then return (and reset to 0) the number of rows found not positive
    definite by half-sweeps since the previous call. */

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libals.so")
 ALS_OK = 0
 ALS_F_MAX = 128
 EXPORTED = ("als_workspace_bytes", "als_init", "als_destroy", "als_half_sweep", "als_rmse",
-            "als_status", "als_plan", "als_csr_to_csc", "als_profile_begin", "als_profile_end",
+            "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_profile_begin", "als_profile_end",
             "als_last_hip_error", "als_strerror")
 
 
@@ -46,13 +46,14 @@ def _load():
     lib.als_status.argtypes = [P, P, ctypes.POINTER(i64)]
     lib.als_plan.argtypes = [P, P, i64, i32, P, i64, P, P]
     lib.als_csr_to_csc.argtypes = [P, P, P, P, i64, i64, P, P, P, P]
+    lib.als_rmse_waves.argtypes = [P, i32]
     lib.als_profile_begin.argtypes = [P, i32]
     lib.als_profile_end.argtypes = [P, P, i32, ctypes.POINTER(i32)]
     lib.als_last_hip_error.argtypes = [P]
     lib.als_strerror.argtypes = [ctypes.c_int]
     lib.als_strerror.restype = ctypes.c_char_p
     for fn in ("als_init", "als_destroy", "als_half_sweep", "als_rmse", "als_status", "als_plan",
-               "als_csr_to_csc", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
+               "als_csr_to_csc", "als_rmse_waves", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
         getattr(lib, fn).restype = ctypes.c_int
     return lib
 
@@ -151,6 +152,12 @@ def als_rmse(ctx: Context, rowptr, colidx, vals, m: int, n: int, f: int, x, thet
                        _dev(out, torch.float64, "out", 1), _stream(ctx.device, stream))
     _check("als_rmse", rc, ctx.handle)
     return out
+
+
+def als_rmse_waves(ctx: Context, waves_per_simd: int):
+    """Cap later als_rmse calls on this context at `waves_per_simd` resident waves per SIMD
+    (0: as many as fit).  The result does not depend on the width."""
+    _check("als_rmse_waves", _lib.als_rmse_waves(ctx.handle, waves_per_simd), ctx.handle)
 
 
 def als_status(ctx: Context, stream=None) -> int:

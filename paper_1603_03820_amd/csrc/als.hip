@@ -1109,63 +1109,76 @@ struct RmseBody {
     }
 };
 
-// RMSE partials: wave w covers entries [nnz w / W, nnz (w+1) / W), row piece by row piece through
-// the gather pipeline (the next piece's index batches load during the current piece); x_u is
-// loaded once per piece.  NB = f / 16 + 1 (the gather's block count).
+// RMSE partials: the entries are cut into C equal chunks, chunk w = [nnz w / C, nnz (w+1) / C);
+// persistent waves claim chunks in order from a counter and walk each row piece by row piece
+// through the gather pipeline (the next piece's index batches load during the current piece;
+// x_u is loaded once per piece).  Chunk w's fp64 sum goes to partial[w], so the result does not
+// depend on how many waves run or which wave took which chunk: the kernel may run at any width,
+// e.g. one wave per SIMD beside a half-sweep.  NB = f / 16 + 1 (the gather's block count).
 template <int NB, bool BUF>
 __global__ __launch_bounds__(kWave) void k_rmse_rows(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, int64_t m, int64_t n, int f, const float* __restrict__ x,
-    const float* __restrict__ theta, int W, double* __restrict__ partial) {
+    const float* __restrict__ theta, int C, double* __restrict__ partial,
+    unsigned* __restrict__ claim) {
     using G = Gather<NB, BUF, 0>;
     __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x, c = lane & 15;
-    const int w = blockIdx.x;
     const int64_t nnz = rowptr[m];
-    const int64_t kb = nnz / W * w + (nnz % W) * w / W;
-    const int64_t ke = nnz / W * (w + 1) + (nnz % W) * (w + 1) / W;
-    double acc = 0.0;
-    if (kb < ke) {
-        int64_t lo = 0, hi = m - 1;   // row of entry kb: largest u < m with rowptr[u] <= kb
-        while (lo < hi) {
-            const int64_t mid = (lo + hi + 1) >> 1;
-            if (rowptr[mid] <= kb) lo = mid; else hi = mid - 1;
-        }
-        int64_t u = lo;
-        int64_t pb = kb, pe = rowptr[u + 1] < ke ? rowptr[u + 1] : ke;
-        const G gat(theta, n, f, c);
-        RowIndex ix;
-        Inflight<G::kBuf> in;
-        gram_prefetch(gat, colidx, vals, pb, pe, lane, ix);
-        gram_stage(gat, ix, ring, lane, in);
-        for (;;) {
-            int64_t un = u + 1;   // the next row with entries in the range
-            while (un < m && rowptr[un] < ke && rowptr[un + 1] == rowptr[un]) ++un;
-            const bool more = un < m && rowptr[un] < ke;
-            int64_t nb0 = 0, nb1 = 0;
-            if (more) {
-                nb0 = rowptr[un];
-                nb1 = rowptr[un + 1] < ke ? rowptr[un + 1] : ke;
-                gram_prefetch(gat, colidx, vals, nb0, nb1, lane, ix);
+    // No lane-0-only region in this loop: every lane takes part in the claim (lane 0 adds one,
+    // the others zero) and every lane stores the wave's sum.  (Two lane-0 regions at the ends of
+    // the loop body were joined across the back edge by the compiler, leaving lanes 1..63 in a
+    // loop of their own that read a stale chunk number.)
+    for (;;) {
+        const unsigned got = atomicAdd(claim, lane == 0 ? 1u : 0u);
+        const int w = __builtin_amdgcn_readfirstlane((int)got);
+        if (w >= C) break;
+        const int64_t kb = nnz / C * w + (nnz % C) * w / C;
+        const int64_t ke = nnz / C * (w + 1) + (nnz % C) * (w + 1) / C;
+        double acc = 0.0;
+        if (kb < ke) {
+            int64_t lo = 0, hi = m - 1;   // row of entry kb: largest u < m with rowptr[u] <= kb
+            while (lo < hi) {
+                const int64_t mid = (lo + hi + 1) >> 1;
+                if (rowptr[mid] <= kb) lo = mid; else hi = mid - 1;
             }
-            float xr[NB];
-#pragma unroll
-            for (int I = 0; I < NB; ++I) {
-                const int j = 16 * I + c;
-                xr[I] = j < f ? x[(size_t)u * (size_t)f + j] : 0.f;
-            }
-            RmseBody<NB, G> body{gat, xr, acc, c == 0, {}, {}, 0.f};
-            pipe_loop(gat, colidx, vals, pb, pe, ring, lane, in, body);
-            if (!more) break;
+            int64_t u = lo;
+            int64_t pb = kb, pe = rowptr[u + 1] < ke ? rowptr[u + 1] : ke;
+            const G gat(theta, n, f, c);
+            RowIndex ix;
+            Inflight<G::kBuf> in;
+            gram_prefetch(gat, colidx, vals, pb, pe, lane, ix);
             gram_stage(gat, ix, ring, lane, in);
-            u = un;
-            pb = nb0;
-            pe = nb1;
+            for (;;) {
+                int64_t un = u + 1;   // the next row with entries in the range
+                while (un < m && rowptr[un] < ke && rowptr[un + 1] == rowptr[un]) ++un;
+                const bool more = un < m && rowptr[un] < ke;
+                int64_t nb0 = 0, nb1 = 0;
+                if (more) {
+                    nb0 = rowptr[un];
+                    nb1 = rowptr[un + 1] < ke ? rowptr[un + 1] : ke;
+                    gram_prefetch(gat, colidx, vals, nb0, nb1, lane, ix);
+                }
+                float xr[NB];
+#pragma unroll
+                for (int I = 0; I < NB; ++I) {
+                    const int j = 16 * I + c;
+                    xr[I] = j < f ? x[(size_t)u * (size_t)f + j] : 0.f;
+                }
+                RmseBody<NB, G> body{gat, xr, acc, c == 0, {}, {}, 0.f};
+                pipe_loop(gat, colidx, vals, pb, pe, ring, lane, in, body);
+                if (!more) break;
+                gram_stage(gat, ix, ring, lane, in);
+                u = un;
+                pb = nb0;
+                pe = nb1;
+            }
         }
+        // only the 16-lane groups' first lanes hold sums: the full butterfly leaves the wave's
+        // total in every lane
+        for (int o = 1; o < kWave; o <<= 1) acc += __shfl_xor(acc, o);
+        partial[w] = acc;
     }
-    acc += __shfl_xor(acc, 16);
-    acc += __shfl_xor(acc, 32);
-    if (lane == 0) partial[w] = acc;
 }
 
 __global__ __launch_bounds__(kWave) void k_rmse_final(const int64_t* __restrict__ rowptr,
@@ -1366,7 +1379,7 @@ Layout make_layout(const int* waves, int nb_max, int cus) {
     }
     Layout L;
     size_t off = 0;
-    L.status = off; off = align256(off + 256);   // non-SPD counter at 0, chunk counter at 64
+    L.status = off; off = align256(off + 256);   // non-SPD counter at 0, chunk counters at 64, 128
     L.bounds = off; off = align256(off + sizeof(int64_t) * 2 * (size_t)(c_cap + 1));
     L.rmse = off;   off = align256(off + sizeof(double) * (size_t)cus * kRmseWavesPerCU);
     L.slots = off;  off = align256(off + slot_bytes);
@@ -1398,20 +1411,23 @@ int occupancy_waves(int cus, int* waves) {
     return 0;
 }
 
-// Launch the RMSE partials kernel with as many resident waves as it fits, up to
-// kRmseWavesPerCU per CU (the partials buffer holds that many); *W gets the wave count.
+// Launch the RMSE partials kernel over C = cus * kRmseWavesPerCU chunks (the partials buffer
+// holds that many) with as many resident waves as fit, at most `cap_per_cu` per CU if that is
+// positive; the claim counter is reset first, on the same stream.
 template <int NB, bool BUF>
-hipError_t rmse_rows_launch(int cus, hipStream_t st, const int64_t* rowptr,
+hipError_t rmse_rows_launch(int cus, int cap_per_cu, hipStream_t st, const int64_t* rowptr,
                             const int32_t* colidx, const float* vals, int64_t m, int64_t n,
-                            int f, const float* x, const float* theta, double* part, int* W) {
+                            int f, const float* x, const float* theta, double* part,
+                            unsigned* claim, int C) {
     int b = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
         &b, (const void*)k_rmse_rows<NB, BUF>, kWave, 0);
     if (e != hipSuccess) return e;
     b = b < 1 ? 1 : (b > kRmseWavesPerCU ? kRmseWavesPerCU : b);
-    *W = cus * b;
-    hipLaunchKernelGGL((k_rmse_rows<NB, BUF>), dim3(*W), dim3(kWave), 0, st, rowptr, colidx,
-                       vals, m, n, f, x, theta, *W, part);
+    if (cap_per_cu > 0 && b > cap_per_cu) b = cap_per_cu;
+    hipLaunchKernelGGL(k_reset_counter, dim3(1), dim3(1), 0, st, (unsigned long long*)claim);
+    hipLaunchKernelGGL((k_rmse_rows<NB, BUF>), dim3(cus * b), dim3(kWave), 0, st, rowptr,
+                       colidx, vals, m, n, f, x, theta, C, part, claim);
     return hipGetLastError();
 }
 
@@ -1469,6 +1485,7 @@ struct als_ctx {
     int prof_count;
     bool global_gather;    // use the 64-bit-load gather for every size (ALS_GATHER=global)
     bool tile_last_block;  // 16x16 tiles for the last block column always (ALS_LAST_BLOCK=tiles)
+    int rmse_waves_per_simd;   // cap on resident RMSE waves per SIMD (0 = as many as fit)
 };
 
 namespace {
@@ -1721,13 +1738,15 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
     hipStream_t st = (hipStream_t)stream;
-    int W = 0;
+    const int C = ctx->cus * kRmseWavesPerCU;
     double* part = (double*)(ctx->ws + ctx->lay.rmse);
+    auto* claim = (unsigned*)(ctx->ws + ctx->lay.status + 128);
     hipError_t le = hipSuccess;
     if (m > 0) {
         const bool buf =
             !ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
-#define ALS_RMSE_ARGS ctx->cus, st, rowptr, colidx, vals, m, n, f, x, theta, part, &W
+#define ALS_RMSE_ARGS ctx->cus, 4 * ctx->rmse_waves_per_simd, st, rowptr, colidx, vals, m, n, f, \
+                      x, theta, part, claim, C
         switch (f / 16 + 1) {
 #define ALS_RMSE_CASE(NB)                                                           \
             case NB:                                                                \
@@ -1742,7 +1761,7 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
         }
         if (le != hipSuccess) return fail_hip(ctx, le);
     }
-    hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? W : 0, part,
+    hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? C : 0, part,
                        rmse_out);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
@@ -1833,6 +1852,13 @@ int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
                            vals, m, n, (int)R, cnt, colptr, rowidx, vals_t);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
+}
+
+int als_rmse_waves(als_ctx* ctx, int32_t waves_per_simd) {
+    if (!ctx || waves_per_simd < 0 || waves_per_simd > kRmseWavesPerCU / 4)
+        return ALS_ERR_INVALID_ARG;
+    ctx->rmse_waves_per_simd = waves_per_simd;
+    return ALS_OK;
 }
 
 int als_last_hip_error(const als_ctx* ctx) { return ctx ? ctx->last_hip : 0; }

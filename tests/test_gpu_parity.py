@@ -298,6 +298,46 @@ def test_rmse_matches_oracle(ctx, ctx_global, orc, form):
         assert abs(out.item() - ref) <= 1e-6 * ref, (form, f, out.item(), ref)
 
 
+def test_rmse_does_not_depend_on_width(orc):
+    """als_rmse at one wave per SIMD (the width that fits beside a half-sweep), at two, and at
+    the default width: bit-identical (fixed chunks, fixed order), and within 1e-6 of the oracle.
+    Also run at width one on a second stream while a half-sweep of another context runs."""
+    from paper_1603_03820_amd import als
+    p = synth.make(20_000, 3_000, 1_500_000, rows="lognormal", zipf=0.9, f=100, model="movie",
+                   seed=35)
+    x = synthetic_factor(p.m, 100, 36, 0.3)
+    th = synthetic_factor(p.n, 100, 37, 0.3)
+    ref = orc.rmse(p.rowptr, p.colidx, p.vals, p.m, 100, x.astype(np.float64),
+                   th.astype(np.float64))
+    c = als.Context(0, 100)
+    dev = c.device
+    rp, ci, v = to_dev(p.rowptr, dev), to_dev(p.colidx, dev), to_dev(p.vals, dev)
+    xd, td = to_dev(x, dev), to_dev(th, dev)
+    got = {}
+    for w in (0, 1, 2, 8):
+        log(f"rmse width {w}")
+        als.als_rmse_waves(c, w)
+        got[w] = als.als_rmse(c, rp, ci, v, p.m, p.n, 100, xd, td).item()
+    assert len({np.float64(g).tobytes() for g in got.values()}) == 1, got
+    assert abs(got[0] - ref) <= 1e-6 * ref, (got[0], ref)
+    # beside a half-sweep on another stream (another context: its own workspace)
+    log("rmse width 1 beside a half-sweep")
+    h = als.Context(0, 100)
+    xo = torch.empty((p.m, 100), dtype=torch.float32, device=dev)
+    side = torch.cuda.Stream(dev)
+    als.als_rmse_waves(c, 1)
+    torch.cuda.synchronize()
+    als.als_half_sweep(h, rp, ci, v, p.m, p.n, 100, p.lam, td, xo)
+    with torch.cuda.stream(side):
+        out = als.als_rmse(c, rp, ci, v, p.m, p.n, 100, xd, td, stream=side)
+    torch.cuda.synchronize()
+    assert np.float64(out.item()).tobytes() == np.float64(got[0]).tobytes()
+    with pytest.raises(als.ALSError):
+        als.als_rmse_waves(c, 9)
+    c.close()
+    h.close()
+
+
 def test_tiny_trajectory_ten_iterations(ctx, orc):
     """Free-running: ten iterations on each side from the same theta0; training RMSE agrees
     within 1e-4 after every iteration."""
