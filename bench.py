@@ -475,6 +475,7 @@ def main():
         theta_ready = [torch.cuda.Event(), torch.cuda.Event()]
         rmse_done = [torch.cuda.Event(), torch.cuda.Event()]
         k_box = [0]
+        last_k = args.warmup + args.steps - 1
 
         def step():
             k = k_box[0]
@@ -485,6 +486,8 @@ def main():
             driver.update_theta(ctx, dp, xk, theta)
             theta_ready[k % 2].record(main_s)
             side_s.wait_event(theta_ready[k % 2])
+            # the last step's RMSE has no update-X beside it: full width
+            als.als_rmse_waves(ctx_r, 0 if k == last_k else 1)
             als.als_rmse(ctx_r, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, xk, theta, rmse,
                          stream=side_s)
             rmse_done[k % 2].record(side_s)
