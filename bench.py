@@ -46,7 +46,7 @@ def F_s(f):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="movie", help="synth config name (movie, tiny, music)")
     ap.add_argument("--f", type=int, default=None, help="rank override (rank sweep)")
