@@ -246,10 +246,9 @@ def driver_bench(args):
     dev = torch.device("cuda", 0)
     p = synth.config(args.config, f=args.f)
     (tr, te) = synth.split(p.rowptr, p.colidx, p.vals, args.test_frac, p.recipe["seed"])
-    csc = synth.transpose(p.m, p.n, *tr)
-    dp = driver.DeviceProblem.from_host(p.m, p.n, p.f, p.lam, *tr, *csc, dev)
-    test = driver.RatingSet.from_host(p.m, p.n, *te, dev)
     ctx = als.Context(0, max(p.f, 16))
+    dp = driver.DeviceProblem.from_host_csr(ctx, p.m, p.n, p.f, p.lam, *tr)   # CSC on the device
+    test = driver.RatingSet.from_host(p.m, p.n, *te, dev)
     th0 = torch.from_numpy(p.theta0).to(dev)
     iters = args.steps
     driver.run(ctx, dp, th0, args.warmup, test=test)             # warm-up

@@ -1082,10 +1082,11 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
 }
 
 // RMSE body: per step, entry slot g's residual r - x_u . theta_v in fp32 (the dot product over
-// the slot's 16 lanes by DPP row sums), squared and added in fp64 by the slot's first lane.  An
-// entry past the piece's end gathers zeros and rating 0, so its residual is 0.  x_u sits in
-// registers: lane (g, c) holds x_u[16 I + c] (0 past f, which also cancels the rating that the
-// gather puts in column f).
+// the slot's 16 lanes by DPP row sums); the squares of a group's kGroup steps are summed in fp32
+// (at most kGroup terms per lane) and that sum is added in fp64 by the slot's first lane at the
+// group's last step.  An entry past the piece's end gathers zeros and rating 0, so its residual
+// is 0.  x_u sits in registers: lane (g, c) holds x_u[16 I + c] (0 past f, which also cancels the
+// rating that the gather puts in column f).
 template <int NB, class G>
 struct RmseBody {
     const G& gat;
@@ -1093,6 +1094,7 @@ struct RmseBody {
     double& acc;
     bool lead;
     float v[NB], w[1], r;
+    float sq;   // this group's squares so far
     __device__ __forceinline__ void take(const float (&B)[G::kBuf], float rr, bool ok) {
         gat.operands(B, rr, ok, v, w);
         r = ok ? rr : 0.f;
@@ -1104,8 +1106,8 @@ struct RmseBody {
         for (int I = 0; I < NB; ++I) d = __builtin_fmaf(v[I], xr[I], d);
         d = row_sum16(d);
         const float e = r - d;
-        const double e2 = (double)e * (double)e;
-        acc += lead ? e2 : 0.0;
+        sq = (J == 0) ? e * e : __builtin_fmaf(e, e, sq);
+        if constexpr (J == kGroup - 1) acc += lead ? (double)sq : 0.0;
     }
 };
 
@@ -1165,7 +1167,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
                     const int j = 16 * I + c;
                     xr[I] = j < f ? x[(size_t)u * (size_t)f + j] : 0.f;
                 }
-                RmseBody<NB, G> body{gat, xr, acc, c == 0, {}, {}, 0.f};
+                RmseBody<NB, G> body{gat, xr, acc, c == 0, {}, {}, 0.f, 0.f};
                 pipe_loop(gat, colidx, vals, pb, pe, ring, lane, in, body);
                 if (!more) break;
                 gram_stage(gat, ix, ring, lane, in);

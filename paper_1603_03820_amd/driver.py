@@ -34,6 +34,15 @@ class DeviceProblem:
         t = lambda a: torch.from_numpy(a).to(device)  # noqa: E731
         return cls(m, n, f, lam, t(rowptr), t(colidx), t(vals), t(colptr), t(rowidx), t(vals_t))
 
+    @classmethod
+    def from_host_csr(cls, ctx, m, n, f, lam, rowptr, colidx, vals):
+        """Upload the CSR of R only; its CSC (the item side's input) is built on the device by
+        als_csr_to_csc (stable, so identical to any stable host transpose)."""
+        t = lambda a: torch.from_numpy(a).to(ctx.device)  # noqa: E731
+        rp, ci, v = t(rowptr), t(colidx), t(vals)
+        colptr, rowidx, vals_t = als.als_csr_to_csc(ctx, rp, ci, v, m, n, nnz=int(rowptr[-1]))
+        return cls(m, n, f, lam, rp, ci, v, colptr, rowidx, vals_t)
+
 
 @dataclass
 class RatingSet:

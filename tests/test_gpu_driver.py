@@ -72,3 +72,18 @@ def test_checkpoint_resume_is_bit_exact(ctx, tmp_path):
     assert torch.equal(x4b, x4) and torch.equal(t4b, t4)
     it, xl, tl = driver.load_checkpoint(str(tmp_path), ctx.device)
     assert it == 6 and torch.equal(xl, x6) and torch.equal(tl, t6)
+
+
+def test_device_built_csc_gives_the_same_run(ctx):
+    """DeviceProblem.from_host_csr builds the item side's CSC with als_csr_to_csc: the same CSC
+    as the host transpose bit for bit, hence the same ten iterations bit for bit."""
+    from paper_1603_03820_amd import driver
+    p, tr, te, csc, dp, test = _problem(ctx)
+    log("tiny: CSC built on the device")
+    dd = driver.DeviceProblem.from_host_csr(ctx, p.m, p.n, p.f, p.lam, *tr)
+    assert torch.equal(dd.colptr, dp.colptr) and torch.equal(dd.rowidx, dp.rowidx)
+    assert torch.equal(dd.vals_t.view(torch.int32), dp.vals_t.view(torch.int32))
+    th0 = to_dev(p.theta0, ctx.device)
+    x1, t1, _ = driver.run(ctx, dp, th0, 3)
+    x2, t2, _ = driver.run(ctx, dd, th0, 3)
+    assert torch.equal(x1, x2) and torch.equal(t1, t2)
