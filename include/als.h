@@ -141,6 +141,24 @@ int als_plan(als_ctx* ctx, const int64_t* rowptr, int64_t m, int32_t f, int64_t*
              int64_t capacity, int64_t* params_out, void* stream);
 
 /*
+ * Test and debug support: the gather stage of the half-sweep (Algorithm 1's read of the theta_v
+ * of a row's rated columns) for row u, made visible.  The same gather form, index pipeline and
+ * operand layout as als_half_sweep with this context and f run over row u, and instead of the
+ * matrix products they write what each entry's operands hold.  With NB = f / 16 + 1, entry k
+ * of the row (k < n_u) gets a record of 16 (NB + 3) floats at out + k 16 (NB + 3):
+ *   [16 I + c]        block I of the MFMA operand, lane c: theta_v[16 I + c] for 16 I + c < f,
+ *                     the rating r at 16 I + c == f, 0 beyond (I < NB);
+ *   [16 (NB + p) + c] the quad-form operand w[p], when the last block column runs in quad form
+ *                     (p < P): theta_v[16 (NB - 1) + 4 p + (c & 3)] for the theta quads, and for
+ *                     the rating quad r at (c & 3) == 0, else 0 (untouched otherwise);
+ *   [16 (NB + 2) + c] the rating r (every c).
+ * Records past capacity (in floats) are not written.  Bit-exact against theta and vals.
+ */
+int als_gather_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
+                    const float* vals, int64_t m, int64_t n, int32_t f, const float* theta,
+                    int64_t u, float* out, int64_t capacity, void* stream);
+
+/*
  * Measurement support (not part of the method).  After als_profile_begin, each of the next
  * `capacity` half-sweeps records HIP events on its own stream around its three kernels (plan,
  * herm_solve, reduce_solve).  als_profile_end synchronises on the last event, writes

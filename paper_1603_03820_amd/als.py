@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libals.so")
 ALS_OK = 0
 ALS_F_MAX = 128
 EXPORTED = ("als_workspace_bytes", "als_init", "als_destroy", "als_half_sweep", "als_rmse",
-            "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_profile_begin", "als_profile_end",
+            "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin", "als_profile_end",
             "als_last_hip_error", "als_strerror")
 
 
@@ -47,13 +47,14 @@ def _load():
     lib.als_plan.argtypes = [P, P, i64, i32, P, i64, P, P]
     lib.als_csr_to_csc.argtypes = [P, P, P, P, i64, i64, P, P, P, P]
     lib.als_rmse_waves.argtypes = [P, i32]
+    lib.als_gather_dump.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, i64, P]
     lib.als_profile_begin.argtypes = [P, i32]
     lib.als_profile_end.argtypes = [P, P, i32, ctypes.POINTER(i32)]
     lib.als_last_hip_error.argtypes = [P]
     lib.als_strerror.argtypes = [ctypes.c_int]
     lib.als_strerror.restype = ctypes.c_char_p
     for fn in ("als_init", "als_destroy", "als_half_sweep", "als_rmse", "als_status", "als_plan",
-               "als_csr_to_csc", "als_rmse_waves", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
+               "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
         getattr(lib, fn).restype = ctypes.c_int
     return lib
 
@@ -207,6 +208,23 @@ def als_csr_to_csc(ctx: Context, rowptr, colidx, vals, m: int, n: int, nnz: int 
                              _stream(ctx.device, stream))
     _check("als_csr_to_csc", rc, ctx.handle)
     return colptr, rowidx[:nnz], vals_t[:nnz]
+
+
+def als_gather_dump(ctx: Context, rowptr, colidx, vals, m: int, n: int, f: int, theta, u: int,
+                    n_u: int, stream=None):
+    """The gather stage of the half-sweep on row u, as a float32 device tensor [n_u, NB + 3, 16]
+    (NB = f // 16 + 1): per entry the MFMA operand blocks, the quad-form operands and the
+    rating (see als_gather_dump in include/als.h).  Zero-filled before the call."""
+    nb = f // 16 + 1
+    out = torch.zeros((max(n_u, 1), nb + 3, 16), dtype=torch.float32, device=ctx.device)
+    rc = _lib.als_gather_dump(ctx.handle, _dev(rowptr, torch.int64, "rowptr", m + 1),
+                              _dev(colidx, torch.int32, "colidx"),
+                              _dev(vals, torch.float32, "vals"), m, n, f,
+                              _dev(theta, torch.float32, "theta", n * f), u,
+                              ctypes.c_void_p(out.data_ptr()), n_u * (nb + 3) * 16,
+                              _stream(ctx.device, stream))
+    _check("als_gather_dump", rc, ctx.handle)
+    return out[:n_u]
 
 
 def als_profile_begin(ctx: Context, capacity: int):

@@ -522,6 +522,62 @@ __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restric
     pipe_loop(gat, colidx, vals, kbeg, kend, ring, lane, in, body);
 }
 
+// The gather stage made visible (test and debug support): for one row, the operands the Gram's
+// MFMAs would receive -- the same Gather form, index ring and pipeline as k_herm_solve -- are
+// written out per entry instead of multiplied.  Entry k's record has 16 (NB + 3) floats: block I
+// of the MFMA operand at 16 I + c (lane c of the entry's 16-lane group), the quad operands w[p] at
+// 16 (NB + p) + c (quad form only; untouched otherwise), and the rating the body uses at
+// 16 (NB + 2) + c.
+template <int NB>
+constexpr int dump_floats() { return 16 * (NB + 3); }
+
+template <int NB, int P, class G>
+struct DumpBody {
+    const G& gat;
+    float* __restrict__ out;
+    int64_t limit;   // entries that fit in out
+    int total, lane, step;
+    float v[NB], w[P > 0 ? P : 1], r;
+    __device__ __forceinline__ void take(const float (&B)[G::kBuf], float rr, bool ok) {
+        gat.operands(B, rr, ok, v, w);
+        r = rr;
+    }
+    template <int J>
+    __device__ __forceinline__ void run() {
+        const int g = lane >> 4, c = lane & 15;
+        const int64_t k = 4 * (int64_t)step + g;
+        if (k < total && k < limit) {
+            float* rec = out + k * dump_floats<NB>();
+#pragma unroll
+            for (int I = 0; I < NB; ++I) rec[16 * I + c] = v[I];
+            if constexpr (P > 0) {
+#pragma unroll
+                for (int p = 0; p < P; ++p) rec[16 * (NB + p) + c] = w[p];
+            }
+            rec[16 * (NB + 2) + c] = r;
+        }
+        ++step;
+    }
+};
+
+template <int NB, bool BUF, int P>
+__global__ __launch_bounds__(kWave) void k_gather_dump(
+    const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    const float* __restrict__ vals, const float* __restrict__ theta, int64_t n, int f, int64_t u,
+    float* __restrict__ out, int64_t limit) {
+    using G = Gather<NB, BUF, P>;
+    __shared__ RingEntry ring[kRing];
+    const int lane = threadIdx.x;
+    const G gat(theta, n, f, lane & 15);
+    const int64_t kbeg = rowptr[u], kend = rowptr[u + 1];
+    RowIndex ix;
+    Inflight<G::kBuf> in;
+    gram_prefetch(gat, colidx, vals, kbeg, kend, lane, ix);
+    gram_stage(gat, ix, ring, lane, in);
+    DumpBody<NB, P, G> body{gat, out, limit, (int)(kend - kbeg), lane, 0, {}, {}, 0.f};
+    pipe_loop(gat, colidx, vals, kbeg, kend, ring, lane, in, body);
+}
+
 // ------------------------------------------------------------------ solve in registers ---
 
 // LDS scratch of one wave for the solve.
@@ -1582,6 +1638,32 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     if (ev) (void)hipEventRecord(ev[3], st);
 }
 
+// The gather form k_herm_solve would use for this call (buffer loads or 64-bit loads; quad form or
+// tiles for the last block column), run by k_gather_dump on row u.
+template <int NB>
+void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
+                 int64_t n, int f, const float* theta, int64_t u, float* out, int64_t limit,
+                 hipStream_t st) {
+    const int f_last = f - 16 * (NB - 1);
+    const int quads =
+        (!ctx->tile_last_block && (f_last == 0 || f_last == 4)) ? f_last / 4 + 1 : 0;
+    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
+        if (quads == 1)
+            hipLaunchKernelGGL((k_gather_dump<NB, true, 1>), dim3(1), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, theta, n, f, u, out, limit);
+        else if (quads == 2) {
+            if constexpr (kQuad2<NB>)
+                hipLaunchKernelGGL((k_gather_dump<NB, true, 2>), dim3(1), dim3(kWave), 0, st,
+                                   rowptr, colidx, vals, theta, n, f, u, out, limit);
+        } else
+            hipLaunchKernelGGL((k_gather_dump<NB, true, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, theta, n, f, u, out, limit);
+    } else {
+        hipLaunchKernelGGL((k_gather_dump<NB, false, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
+                           colidx, vals, theta, n, f, u, out, limit);
+    }
+}
+
 void profile_free(als_ctx* ctx) {
     if (!ctx->prof_ev) return;
     for (int i = 0; i < 4 * ctx->prof_cap; ++i) (void)hipEventDestroy(ctx->prof_ev[i]);
@@ -1852,6 +1934,36 @@ int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
     if (m > 0 && n > 0)
         hipLaunchKernelGGL(k_tr_scatter, dim3((unsigned)R), dim3(kWave), 0, st, rowptr, colidx,
                            vals, m, n, (int)R, cnt, colptr, rowidx, vals_t);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
+}
+
+int als_gather_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
+                    const float* vals, int64_t m, int64_t n, int32_t f, const float* theta,
+                    int64_t u, float* out, int64_t capacity, void* stream) {
+    if (!ctx) return ALS_ERR_INVALID_ARG;
+    if (f < 1 || f > ctx->f_max) return ALS_ERR_UNSUPPORTED_F;
+    if (m < 1 || n < 0 || u < 0 || u >= m || capacity < 0 || !rowptr || !out)
+        return ALS_ERR_INVALID_ARG;
+    if (n > 0 && (!colidx || !vals || !theta)) return ALS_ERR_INVALID_ARG;
+    if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(vals, 4) || !aligned(theta, 4) ||
+        !aligned(out, 4))
+        return ALS_ERR_ALIGN;
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return ALS_ERR_DEVICE;
+    hipStream_t st = (hipStream_t)stream;
+    const int nb = nb_of(f);
+    const int64_t limit = capacity / (16 * (nb + 3));
+    switch (nb) {
+#define ALS_DUMP_CASE(NB)                                                                     \
+        case NB:                                                                              \
+            launch_dump<NB>(ctx, rowptr, colidx, vals, n, f, theta, u, out, limit, st);       \
+            break;
+        ALS_DUMP_CASE(1) ALS_DUMP_CASE(2) ALS_DUMP_CASE(3) ALS_DUMP_CASE(4) ALS_DUMP_CASE(5)
+        ALS_DUMP_CASE(6) ALS_DUMP_CASE(7) ALS_DUMP_CASE(8) ALS_DUMP_CASE(9)
+#undef ALS_DUMP_CASE
+        default: return ALS_ERR_UNSUPPORTED_F;
+    }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
 }
