@@ -84,3 +84,74 @@ def test_peak_microbenchmarks_build_and_export():
     assert not scalar_writes.search(text)
     assert not re.search(r"\bv_pk_(?:add|mul|fma)_f32", text)
     assert "v_mfma_f32_16x16x4_f32" in text and "v_fma_f32" in text
+
+
+def _vgprs(tok):
+    m = re.match(r"v\[(\d+):(\d+)\]", tok)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", tok)
+    return {int(m.group(1))} if m else set()
+
+
+def dpp_violations(text):
+    """DPP instructions whose source VGPR (src0) a VALU instruction wrote less than two wait
+    states earlier (s_nop N counts N + 1).  The DPP FMAs of the factorisation are inline
+    assembly, so the compiler does not insert these wait states itself.  A linear scan per
+    function: every textual predecessor counts, whichever way control reaches the DPP op."""
+    bad, hist = [], []
+    for line in text.splitlines():
+        t = line.split("//")[0].strip()
+        if t.endswith(">:"):
+            hist = []
+            continue
+        if not t or t.endswith(":"):
+            continue
+        op = t.split()[0]
+        if op == "s_nop":
+            hist.append((set(), int(t.split()[1], 0) + 1))
+            continue
+        args = [a.strip() for a in t[len(op):].split(",")]
+        if "_dpp" in op and len(args) > 1:
+            src, ws = _vgprs(args[1].split()[0]), 0
+            for written, n in reversed(hist):
+                if ws >= 2:
+                    break
+                if written & src:
+                    bad.append(t)
+                    break
+                ws += n
+        written = set()
+        if (op.startswith("v_") and not op.startswith(("v_readlane", "v_readfirstlane", "v_cmp"))
+                and args and args[0]):
+            written = _vgprs(args[0].split()[0])
+        hist = (hist + [(written, 1)])[-8:]
+    return bad
+
+
+def test_dpp_sources_settled():
+    """Every DPP instruction in the library reads its source at least two wait states after the
+    source's last VALU write (the rule the factorisation's inline DPP FMAs keep by hand), and the
+    check itself catches a planted violation."""
+    if not os.path.exists("/opt/rocm/llvm/bin/clang-offload-bundler"):
+        pytest.skip("ROCm LLVM tools not installed")
+    text = _device_disassembly()
+    assert text.count("_dpp") > 1000
+    assert dpp_violations(text) == []
+    planted = ("<k>:\n\tv_mul_f32_e32 v5, v1, v2\n"
+               "\tv_fmac_f32_dpp v4, v5, v30 row_newbcast:1 row_mask:0xf bank_mask:0xf\n"
+               "\tv_mul_f32_e32 v6, v1, v2\n\ts_nop 1\n"
+               "\tv_fmac_f32_dpp v4, v6, v30 row_newbcast:1 row_mask:0xf bank_mask:0xf\n")
+    assert len(dpp_violations(planted)) == 1
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py --gpus N > 1 exits with a message before touching a GPU."""
+    import json
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    msg = json.loads(r.stdout.strip().splitlines()[-1])
+    assert msg["n_gpus"] == 2 and "one GPU" in msg["error"]
