@@ -1390,6 +1390,93 @@ __global__ __launch_bounds__(256) void k_scan_apply(int64_t* __restrict__ a, int
     }
 }
 
+// LDS forms of the count and the scatter, for n <= kTrLdsCols: the block's per-column counters
+// (cursors) live in the workgroup's LDS.  Counting: one workgroup of 256 per row block adds its
+// entries into LDS and writes the n counts out.  Scatter: one wave per row block loads
+// colptr[v] + cnt[b][v] into LDS and walks its rows in order; a wave's LDS atomics are performed
+// in issue order, so a column's entries again arrive in row order.
+constexpr int kTrLdsCols = 40960;   // 160 KB of int32 counters
+
+__global__ __launch_bounds__(256) void k_tr_count_lds(const int64_t* __restrict__ rowptr,
+                                                      const int32_t* __restrict__ colidx,
+                                                      int64_t m, int n, int R,
+                                                      int32_t* __restrict__ cnt) {
+    extern __shared__ int32_t lcnt[];
+    const int b = blockIdx.x;
+    for (int v = threadIdx.x; v < n; v += 256) lcnt[v] = 0;
+    __syncthreads();
+    const int64_t k0 = rowptr[tr_row_begin(rowptr, m, R, b)];
+    const int64_t k1 = rowptr[tr_row_begin(rowptr, m, R, b + 1)];
+    for (int64_t k = k0 + threadIdx.x; k < k1; k += 256) {
+        const int32_t v = colidx[k];
+        if (v >= 0 && v < n) atomicAdd(&lcnt[v], 1);
+    }
+    __syncthreads();
+    int32_t* row = cnt + (size_t)b * (size_t)n;
+    for (int v = threadIdx.x; v < n; v += 256) row[v] = lcnt[v];
+}
+
+__global__ __launch_bounds__(kWave) void k_tr_scatter_lds(
+    const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    const float* __restrict__ vals, int64_t m, int n, int R, const int32_t* __restrict__ cnt,
+    const int64_t* __restrict__ colptr, int32_t* __restrict__ rowidx,
+    float* __restrict__ vals_t) {
+    // cur[v]: where this block's next entry of column v goes -- its absolute position when
+    // nnz < 2^31 (then no colptr read per entry), else its position within column v's run
+    extern __shared__ int32_t cur[];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const bool absolute = rowptr[m] <= (int64_t)INT32_MAX;
+    const int32_t* row = cnt + (size_t)b * (size_t)n;
+    for (int v = lane; v < n; v += kWave)
+        cur[v] = absolute ? (int32_t)(colptr[v] + row[v]) : row[v];
+    __syncthreads();
+    const int64_t u0 = tr_row_begin(rowptr, m, R, b), u1 = tr_row_begin(rowptr, m, R, b + 1);
+    // chunks of up to 64 entries of one row, in order; the next chunk's column indices and
+    // ratings load while this one is placed (a chunk never spans two rows, so the lanes of one
+    // LDS atomic never share a column)
+    int64_t u = u0, ks = 0, ke = 0;
+    auto next_chunk = [&](int64_t& cu, int64_t& cs, int64_t& ce) {
+        if (cs + kWave < ce) {
+            cs += kWave;
+            return;
+        }
+        for (++cu; cu < u1; ++cu) {
+            cs = rowptr[cu];
+            ce = rowptr[cu + 1];
+            if (cs < ce) return;
+        }
+    };
+    u = u0 - 1;
+    next_chunk(u, ks, ke);   // the first chunk (ks + kWave >= ke = 0 starts the row walk)
+    int32_t v = -1;
+    float r = 0.f;
+    if (u < u1 && ks + lane < ke) {
+        v = colidx[ks + lane];
+        r = vals[ks + lane];
+    }
+    while (u < u1) {
+        int64_t nu = u, ns = ks, ne = ke;
+        next_chunk(nu, ns, ne);
+        int32_t nv = -1;
+        float nr = 0.f;
+        if (nu < u1 && ns + lane < ne) {
+            nv = colidx[ns + lane];
+            nr = vals[ns + lane];
+        }
+        if (ks + lane < ke && v >= 0 && v < n) {
+            const int32_t at = atomicAdd(&cur[v], 1);
+            const int64_t pos = absolute ? (int64_t)at : colptr[v] + at;
+            rowidx[pos] = (int32_t)u;
+            vals_t[pos] = r;
+        }
+        u = nu;
+        ks = ns;
+        ke = ne;
+        v = nv;
+        r = nr;
+    }
+}
+
 // One wave per row block, its rows in order: each entry goes to colptr[v] + cnt[b][v], which
 // then moves on by one.  The columns of one row are distinct, so the lanes of a row never share
 // a counter; the fence after each row orders its counter updates before the next row's.
@@ -1544,6 +1631,7 @@ struct als_ctx {
     bool global_gather;    // use the 64-bit-load gather for every size (ALS_GATHER=global)
     bool tile_last_block;  // 16x16 tiles for the last block column always (ALS_LAST_BLOCK=tiles)
     int rmse_waves_per_simd;   // cap on resident RMSE waves per SIMD (0 = as many as fit)
+    size_t lds_per_block;      // the device's LDS bytes per workgroup
 };
 
 namespace {
@@ -1566,13 +1654,15 @@ struct DeviceGuard {
     }
 };
 
-int query_device(int device, int f_max, int* cus, int* waves, int* w_cap) {
+int query_device(int device, int f_max, int* cus, int* waves, int* w_cap,
+                 size_t* lds_per_block = nullptr) {
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) return ALS_ERR_DEVICE;
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, device) != hipSuccess) return ALS_ERR_DEVICE;
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return ALS_ERR_DEVICE;
     *cus = prop.multiProcessorCount;
+    if (lds_per_block) *lds_per_block = prop.sharedMemPerBlock;
     DeviceGuard guard(device);
     if (!guard.ok) return ALS_ERR_DEVICE;
     *w_cap = 1;
@@ -1691,7 +1781,8 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
     if (!aligned(workspace, 256)) return ALS_ERR_ALIGN;
     als_ctx* ctx = new (std::nothrow) als_ctx();
     if (!ctx) return ALS_ERR_INVALID_ARG;
-    int rc = query_device(device, f_max, &ctx->cus, ctx->waves, &ctx->w_cap);
+    int rc = query_device(device, f_max, &ctx->cus, ctx->waves, &ctx->w_cap,
+                          &ctx->lds_per_block);
     if (rc != ALS_OK) { delete ctx; return rc; }
     ctx->device = device;
     ctx->f_max = f_max;
@@ -1920,9 +2011,27 @@ int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
         hipLaunchKernelGGL(k_tr_zero, dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, st,
                            cnt, cells);
     }
-    if (m > 0 && n > 0)
-        hipLaunchKernelGGL(k_tr_count, dim3((unsigned)R), dim3(256), 0, st, rowptr, colidx, m, n,
-                           (int)R, cnt);
+    // LDS counters when one row block's fit in a workgroup's LDS
+    const size_t lds_bytes = sizeof(int32_t) * (size_t)(n > 0 ? n : 1);
+    bool lds = n <= kTrLdsCols && lds_bytes <= ctx->lds_per_block;
+    if (lds && m > 0 && n > 0) {
+        hipError_t ea = hipFuncSetAttribute((const void*)k_tr_count_lds,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            (int)lds_bytes);
+        if (ea == hipSuccess)
+            ea = hipFuncSetAttribute((const void*)k_tr_scatter_lds,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+        if (ea != hipSuccess) return fail_hip(ctx, ea);
+    }
+    if (m > 0 && n > 0) {
+        if (lds)
+            hipLaunchKernelGGL(k_tr_count_lds, dim3((unsigned)R), dim3(256),
+                               sizeof(int32_t) * (size_t)n, st, rowptr, colidx, m, (int)n, (int)R,
+                               cnt);
+        else
+            hipLaunchKernelGGL(k_tr_count, dim3((unsigned)R), dim3(256), 0, st, rowptr, colidx,
+                               m, n, (int)R, cnt);
+    }
     if (n > 0)
         hipLaunchKernelGGL(k_tr_colscan, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, n,
                            (int)R, cnt, colptr);
@@ -1931,9 +2040,15 @@ int als_csr_to_csc(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, sums, (int64_t)tiles, colptr, n);
     if (n > 0)
         hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)tiles), dim3(256), 0, st, colptr, n, sums);
-    if (m > 0 && n > 0)
-        hipLaunchKernelGGL(k_tr_scatter, dim3((unsigned)R), dim3(kWave), 0, st, rowptr, colidx,
-                           vals, m, n, (int)R, cnt, colptr, rowidx, vals_t);
+    if (m > 0 && n > 0) {
+        if (lds)
+            hipLaunchKernelGGL(k_tr_scatter_lds, dim3((unsigned)R), dim3(kWave),
+                               sizeof(int32_t) * (size_t)n, st, rowptr, colidx, vals, m, (int)n,
+                               (int)R, cnt, colptr, rowidx, vals_t);
+        else
+            hipLaunchKernelGGL(k_tr_scatter, dim3((unsigned)R), dim3(kWave), 0, st, rowptr,
+                               colidx, vals, m, n, (int)R, cnt, colptr, rowidx, vals_t);
+    }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
 }
