@@ -61,7 +61,7 @@ typedef struct als_ctx als_ctx;
 /* Bytes of device workspace a context on `device` needs for every f <= f_max.  Returns 0 if
    the device cannot be queried or f_max is outside [1, ALS_F_MAX].  The size depends on the
    device's compute-unit count and f_max only (not on m, n or nnz); it is dominated by two
-   partial-accumulator slots per work chunk (about 0.6 GB on a 256-CU MI355X at f_max = 128). */
+   partial-accumulator slots per work chunk (about 1.4 GB on a 256-CU MI355X at f_max = 128). */
 size_t als_workspace_bytes(int device, int32_t f_max);
 
 /* Create a context on `device` using the caller's device workspace (at least

@@ -6,7 +6,7 @@
 //
 // Design (one wave = one worker):
 //   k_plan          integer partition of the rows (and of long rows' entries) into chunks of a
-//                   cost axis: W large chunks, then 4W small ones (see als_plan in als.h); no
+//                   cost axis: W large chunks, then 8W small ones (see als_plan in als.h); no
 //                   host synchronisation needed.
 //   k_herm_solve    persistent waves claim chunks in order and walk their row pieces; gather
 //                   theta_v for four entries at a time straight into MFMA operand registers
@@ -49,7 +49,7 @@ constexpr int kMaxNB = ALS_F_MAX / 16 + 1;      // 9 column blocks of 16 cover f
 constexpr int kSnap = 256;                      // partition cut grid (entries)
 constexpr int kCostPerEntry = 16;               // c_nnz
 constexpr int kTailDiv = 8;                     // the small chunks cover floor(T / 8) of the cost
-constexpr int kSmallPerWave = 4;                // small chunks per wave
+constexpr int kSmallPerWave = 8;                // small chunks per wave
 constexpr int chunks_of(int waves) { return waves * (1 + kSmallPerWave); }
 constexpr int kMaxWavesPerCU = 32;
 constexpr int kRmseWavesPerCU = 32;                // RMSE: up to 8 waves per SIMD (occupancy)
