@@ -1037,24 +1037,46 @@ __device__ __forceinline__ bool cuts_row(const int64_t* __restrict__ rowptr, int
     return u < m && k > 0 && k < rowptr[u + 1] - rowptr[u];
 }
 
-// First and last boundary in [1, C-1] that cut row u, given that boundary b does.
+// First and last boundary in [1, C-1] that cut row u, given that boundary b does.  Boundaries
+// with row u and an offset strictly inside it form one run around b (bounds are sorted by (row,
+// offset): one of row u at offset 0 precedes the run, one at n_u follows it).  Most runs hold one
+// or two boundaries, so each end is found by galloping out from b (steps 1, 2, 4, ...) and then
+// bisecting the last step: a few dependent loads for a short run instead of a bisection of all C.
 __device__ __forceinline__ void cut_range(const int64_t* __restrict__ rowptr, int64_t m,
                                           const int64_t* __restrict__ bounds, int C, int b,
                                           int64_t u, int& b_first, int& b_last) {
-    // boundaries with row u and an offset strictly inside it form one run around b (bounds are
-    // sorted by (row, offset): one of row u at offset 0 precedes the run, one at n_u follows it)
-    int lo = 1, hi = b;   // first boundary >= 1 in the run
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (bounds[2 * mid] < u || !cuts_row(rowptr, m, bounds, mid)) lo = mid + 1; else hi = mid;
+    const auto in_run = [&](int x) { return bounds[2 * x] == u && cuts_row(rowptr, m, bounds, x); };
+    int in = b, out = 0;   // in the run / below it (0: no boundary below the range)
+    for (int d = 1;; d <<= 1) {
+        const int x = b - d;
+        if (x < 1) break;
+        if (!in_run(x)) {
+            out = x;
+            break;
+        }
+        in = x;
     }
-    b_first = lo;
-    lo = b; hi = C - 1;   // last boundary <= C-1 in the run
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (bounds[2 * mid] == u && cuts_row(rowptr, m, bounds, mid)) lo = mid; else hi = mid - 1;
+    while (in - out > 1) {
+        const int mid = (in + out) >> 1;
+        if (in_run(mid)) in = mid; else out = mid;
     }
-    b_last = lo;
+    b_first = in;
+    in = b;
+    out = C;               // above the run (C: no boundary above the range)
+    for (int d = 1;; d <<= 1) {
+        const int x = b + d;
+        if (x > C - 1) break;
+        if (!in_run(x)) {
+            out = x;
+            break;
+        }
+        in = x;
+    }
+    while (out - in > 1) {
+        const int mid = (in + out) >> 1;
+        if (in_run(mid)) in = mid; else out = mid;
+    }
+    b_last = in;
 }
 
 // Add the non-empty boundary pieces of row u for boundaries bb in [from, to] into acc.
