@@ -6,8 +6,9 @@ ratings, f = 100, lambda = 0.05): update-X (half-sweep on the CSR), update-Theta
 on the CSC) and the training RMSE, all through the C ABI of include/als.h.  Inputs are
 resident in HBM before the timed region.  `value` = half-sweeps per second over the K timed
 steps (2 per step).  Step k's RMSE (it reads X_k and Theta_k) runs on a second stream, one wave
-per SIMD, beside step k+1's update-X (which only reads Theta_k; X is double-buffered), and
-step k+1's update-Theta waits for it; --serial-rmse runs it after update-Theta instead.
+per SIMD, beside step k+1 (which only reads Theta_k; X and Theta are double-buffered), and
+step k+2, which overwrites X_k and Theta_k, waits for it; --serial-rmse runs it after
+update-Theta instead.
 
 After the timed region: peak microbenchmarks (FP32 MFMA and VALU FMA rates, an HBM copy) for
 measured denominators, then the fp64 CPU oracle on a bounded row sample (all host threads, plus
@@ -463,14 +464,16 @@ def main():
         return
 
     if not args.serial_rmse:
-        # step k: X_k <- update-X(Theta_{k-1}) into xs[k % 2]; Theta_k <- update-Theta(X_k), once
-        # RMSE_{k-1} (which reads Theta_{k-1}) is done; then RMSE_k(X_k, Theta_k) on the side
-        # stream, where it overlaps update-X of step k+1 (which only reads Theta_k)
+        # step k: X_k <- update-X(Theta_{k-1}) into xs[k % 2]; Theta_k <- update-Theta(X_k) into
+        # ths[k % 2]; then RMSE_k(X_k, Theta_k) on the side stream, where it overlaps step k+1
+        # (which only reads Theta_k and writes the other buffers).  Both factors are double-
+        # buffered, so only step k+2, which overwrites X_k and Theta_k, waits for RMSE_k.
         ctx_r = als.Context(0, max(f, 16))
         als.als_rmse_waves(ctx_r, 1)
         main_s = torch.cuda.current_stream(dev)
         side_s = torch.cuda.Stream(dev)
         xs = [x, torch.empty_like(x)]
+        ths = [torch.empty_like(theta), theta]   # Theta_{-1} (the initial factor) in ths[1]
         theta_ready = [torch.cuda.Event(), torch.cuda.Event()]
         rmse_done = [torch.cuda.Event(), torch.cuda.Event()]
         k_box = [0]
@@ -478,16 +481,16 @@ def main():
 
         def step():
             k = k_box[0]
-            xk = xs[k % 2]
-            driver.update_x(ctx, dp, theta, xk)
-            if k > 0:
-                main_s.wait_event(rmse_done[(k - 1) % 2])
-            driver.update_theta(ctx, dp, xk, theta)
+            xk, th_k = xs[k % 2], ths[k % 2]
+            if k >= 2:
+                main_s.wait_event(rmse_done[k % 2])
+            driver.update_x(ctx, dp, ths[(k - 1) % 2], xk)
+            driver.update_theta(ctx, dp, xk, th_k)
             theta_ready[k % 2].record(main_s)
             side_s.wait_event(theta_ready[k % 2])
             # the last step's RMSE has no update-X beside it: full width
             als.als_rmse_waves(ctx_r, 0 if k == last_k else 1)
-            als.als_rmse(ctx_r, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, xk, theta, rmse,
+            als.als_rmse(ctx_r, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, xk, th_k, rmse,
                          stream=side_s)
             rmse_done[k % 2].record(side_s)
             k_box[0] = k + 1
