@@ -84,9 +84,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_herm_solve_movie_f100_traffic.t
 KERNEL_SRC = os.path.join(ROOT, "paper_1603_03820_amd", "csrc", "als.hip")
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per k_herm_solve launch from the committed counter summary, if it was taken on
-    the kernel source as it is now (else None)."""
+    this workload and on the kernel source as it is now (else None)."""
     import hashlib
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -96,7 +96,8 @@ def measured_traffic():
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if kv.get("source_sha256") != src or "bytes_per_launch" not in kv:
+    if (kv.get("source_sha256") != src or kv.get("workload") != workload
+            or "bytes_per_launch" not in kv):
         return None
     return float(kv["bytes_per_launch"])
 
@@ -537,11 +538,12 @@ def main():
     sweep_ms = plan_ms + herm_ms + red_ms                              # per half-sweep, [step, side]
     herm_avg_fl = float(np.mean(herm_fl))
     achieved = herm_avg_fl / (herm_avg_ms * 1e-3) / 1e12
+    workload = f"{p.name}: m={p.m} n={p.n} nnz={nnz} f={f} lambda={p.lam}"
     roofline = {
         "kernel": f"k_herm_solve<{(f + 15) // 16}> (Gram via fp32 MFMA + in-register Cholesky)",
         "bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS,
         "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
-        "traffic": measured_traffic(),
+        "traffic": measured_traffic(workload),
         "avg_launch_ms": round(herm_avg_ms, 4),
         "flops_per_launch": herm_avg_fl,
     }
@@ -559,7 +561,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{p.name}: m={p.m} n={p.n} nnz={nnz} f={f} lambda={p.lam}",
+        "config": {"workload": workload,
                    "m": p.m, "n": p.n, "nnz": nnz, "f": f, "lambda": p.lam,
                    "step": "update-X + update-Theta + training RMSE" + (
                        " (each RMSE on a second stream, beside the next update-X)"
