@@ -155,3 +155,25 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2
     msg = json.loads(r.stdout.strip().splitlines()[-1])
     assert msg["n_gpus"] == 2 and "one GPU" in msg["error"]
+
+
+def test_bench_traffic_is_tied_to_workload_and_source():
+    """bench.py reports the committed HBM-traffic figure only for the workload the counters were
+    taken on, and only while the kernel source is the one they were taken on."""
+    import hashlib
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    kv = {}
+    for line in open(bench.TRAFFIC_FILE):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    workload = kv["workload"]
+    assert workload.startswith("movie:") and "f=100" in workload
+    same_src = kv["source_sha256"] == hashlib.sha256(open(bench.KERNEL_SRC, "rb").read()).hexdigest()
+    expect = float(kv["bytes_per_launch"]) if same_src else None
+    assert bench.measured_traffic(workload) == expect
+    assert bench.measured_traffic(workload.replace("f=100", "f=32")) is None
+    assert bench.measured_traffic(workload.replace("movie", "music")) is None
