@@ -88,9 +88,9 @@ int als_destroy(als_ctx* ctx);
  *   lambda               : >= 0 and finite
  * Rows with no stored entry get x_u = 0 (the paper does not define them; J does not depend
  * on such an x_u).  A row whose A_u is not numerically positive definite (possible only when
- * lambda = 0 or through overflow) gets NaN in x_u and is counted in the device counter that
- * als_status reports.  The result does not depend on the stream, on earlier calls or on timing:
- * the summation order is fixed.
+ * lambda = 0 or through overflow: a Cholesky pivot that is not positive, is NaN or is +inf)
+ * gets NaN in x_u and is counted in the device counter that als_status reports.  The result
+ * does not depend on the stream, on earlier calls or on timing: the summation order is fixed.
  */
 int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
                    const float* vals, int64_t m, int64_t n, int32_t f, float lambda,
@@ -100,8 +100,10 @@ int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
  * Training root-mean-square error over the stored entries (the evaluation metric of the
  * paper's experiments, on the training set):
  *   *rmse_out = sqrt( sum over stored (u,v) of (r_uv - x_u . theta_v)^2 / nnz )
- * Residuals in fp32, sums in fp64 in a fixed order (per chunk of entries, then over the
- * chunks).  rmse_out is a DEVICE double; 0 when nnz = 0.
+ * Residuals in fp32.  The squares of an entry slot's four consecutive pipeline steps (at most
+ * four terms) are summed in fp32; those group sums are accumulated in fp64 per fixed chunk of
+ * entries, and the chunk sums are added in fp64 in a fixed order.  rmse_out is a DEVICE
+ * double; 0 when nnz = 0.
  */
 int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
              int64_t m, int64_t n, int32_t f, const float* x, const float* theta,

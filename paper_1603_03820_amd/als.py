@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(_PKG, "libals.so")
 ALS_OK = 0
 ALS_F_MAX = 128
 EXPORTED = ("als_workspace_bytes", "als_init", "als_destroy", "als_half_sweep", "als_rmse",
-            "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin", "als_profile_end",
-            "als_last_hip_error", "als_strerror")
+            "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_gather_dump",
+            "als_profile_begin", "als_profile_end", "als_last_hip_error", "als_strerror")
 
 
 class ALSError(RuntimeError):
@@ -54,7 +54,8 @@ def _load():
     lib.als_strerror.argtypes = [ctypes.c_int]
     lib.als_strerror.restype = ctypes.c_char_p
     for fn in ("als_init", "als_destroy", "als_half_sweep", "als_rmse", "als_status", "als_plan",
-               "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin", "als_profile_end", "als_last_hip_error"):
+               "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin",
+               "als_profile_end", "als_last_hip_error"):
         getattr(lib, fn).restype = ctypes.c_int
     return lib
 

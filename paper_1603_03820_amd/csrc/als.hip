@@ -657,8 +657,8 @@ __device__ __forceinline__ void factor_pivot(FactorRegs& R, bool live, int& pmin
 // pivot would make the register allocator copy DPP sources right before their reads); rows of W
 // past npiv stay as the updates left them (the identity in the padding, zero for a pivot skipped
 // inside a block).  In the last block the row nlast is the augmented b row, whose L entries are y
-// (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot was positive (and not
-// NaN) iff pmin > 0 and pmax <= the bits of +inf.
+// (written to S.y).  pmin/pmax track the pivots' bit patterns: every pivot was positive and
+// finite (not NaN, not +inf) iff pmin > 0 and pmax < the bits of +inf.
 // kFull = false: the tile has at most 4 real rows (the last block when f - 16 (NB - 1) <= 4).
 // Then the rows past the first block are neither pivots nor needed (the b row's L entries come
 // from the pivot rows' column nlast), so only block 0 is factored and rows 4..15 of -W are
@@ -856,7 +856,7 @@ __device__ __forceinline__ bool solve_core(f4 (&acc)[ntiles(NB)], int f, float l
         __syncthreads();
         panel_update<NB>(K, acc, S, nlast, lane);
     }
-    const bool ok = pmin > 0 && pmax <= 0x7F800000;
+    const bool ok = pmin > 0 && pmax < 0x7F800000;   // every pivot positive and finite
     // back substitution, last block first; x is zero past f (b column and padding).  Lane
     // (g, c < 4) finishes entry kk = 4g + c of the block (the transposed row sums put it there);
     // with -W_K in S.W, it works with -z.
@@ -944,10 +944,14 @@ void k_herm_solve(
     __shared__ RingEntry ring[kRing];
     const int lane = threadIdx.x;
     const Gather<NB, BUF, P> gat(theta, n, f, lane & 15);
+    // No lane-0-only region in the claim loop: every lane takes part in the claim (lane 0 adds
+    // one, the others zero), and the wave's count of non-SPD rows stays in a register until the
+    // loop has ended (a lane-0 region at each end of a loop body can be joined across the back
+    // edge, leaving lanes 1..63 in a loop of their own).
+    unsigned bad = 0;
     for (;;) {
-        int claim = 0;
-        if (lane == 0) claim = (int)atomicAdd(chunk_ctr, 1u);
-        const int c = __builtin_amdgcn_readfirstlane(claim);
+        const unsigned got = atomicAdd(chunk_ctr, lane == 0 ? 1u : 0u);
+        const int c = __builtin_amdgcn_readfirstlane((int)got);
         if (c >= C) break;
         const int64_t u0 = bounds[2 * c], k0 = bounds[2 * c + 1];
         const int64_t u1 = bounds[2 * c + 2], k1 = bounds[2 * c + 3];
@@ -1006,9 +1010,7 @@ void k_herm_solve(
             if (cur.whole) {
                 const int64_t nu = cur.end - cur.beg;
                 const float lam_n = (float)((double)lambda * (double)nu);
-                if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)cur.u * f, lane) &&
-                    lane == 0)
-                    atomicAdd(nonspd, 1ull);
+                if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)cur.u * f, lane)) ++bad;
             } else {
                 const int which = (cur.u == u0) ? 0 : 1;
                 store_slot<NB>(acc, slots + (size_t)(2 * c + which) * slot_floats(NB), lane);
@@ -1018,6 +1020,8 @@ void k_herm_solve(
             cur = nxt;
         }
     }
+    bad = __builtin_amdgcn_readfirstlane(bad);
+    if (bad) atomicAdd(nonspd, lane == 0 ? (unsigned long long)bad : 0ull);
 }
 
 // Rows cut by chunk boundaries.  Row u's pieces are: the first, held by chunk b_first - 1 (as
@@ -1120,8 +1124,7 @@ template <int NB>
 __device__ __forceinline__ void reduce_row(const int64_t* __restrict__ rowptr, int64_t m, int C,
                                            int f, float lambda, const int64_t* __restrict__ bounds,
                                            float* __restrict__ x_out,
-                                           const float* __restrict__ slots,
-                                           unsigned long long* __restrict__ nonspd,
+                                           const float* __restrict__ slots, unsigned& bad,
                                            SolveLds<NB>& lds, int b, int lane) {
     if (!cuts_row(rowptr, m, bounds, b)) return;
     const int64_t u = bounds[2 * b];
@@ -1144,8 +1147,7 @@ __device__ __forceinline__ void reduce_row(const int64_t* __restrict__ rowptr, i
             add_slot<NB>(acc, slots + (size_t)(2 * g) * slot_floats(NB), lane);
     }
     const float lam_n = (float)((double)lambda * (double)nu);
-    if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane) && lane == 0)
-        atomicAdd(nonspd, 1ull);
+    if (!solve_row<NB>(acc, f, lam_n, lds, x_out + (size_t)u * f, lane)) ++bad;
 }
 
 template <int NB>
@@ -1154,9 +1156,12 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
     const int64_t* __restrict__ bounds, float* __restrict__ x_out,
     const float* __restrict__ slots, unsigned long long* __restrict__ nonspd) {
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
+    const int lane = threadIdx.x;
+    unsigned bad = 0;   // non-SPD rows of this wave, added once after the loop
     for (int b = blockIdx.x + 1; b < C; b += gridDim.x)
-        reduce_row<NB>(rowptr, m, C, f, lambda, bounds, x_out, slots, nonspd, lds, b,
-                       threadIdx.x);
+        reduce_row<NB>(rowptr, m, C, f, lambda, bounds, x_out, slots, bad, lds, b, lane);
+    bad = __builtin_amdgcn_readfirstlane(bad);
+    if (bad) atomicAdd(nonspd, lane == 0 ? (unsigned long long)bad : 0ull);
 }
 
 // RMSE body: per step, entry slot g's residual r - x_u . theta_v in fp32 (the dot product over
@@ -1776,6 +1781,49 @@ void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, con
     }
 }
 
+int rmse_check(const int64_t* rowptr, const int32_t* colidx, const float* vals, int64_t m,
+               int64_t n, int32_t f, const float* x, const float* theta, const double* rmse_out) {
+    if (f < 1 || f > ALS_F_MAX) return ALS_ERR_UNSUPPORTED_F;
+    if (m < 0 || n < 0 || !rowptr || !rmse_out) return ALS_ERR_INVALID_ARG;
+    if (m > 0 && (!x || (n > 0 && (!colidx || !vals || !theta)))) return ALS_ERR_INVALID_ARG;
+    if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(vals, 4) || !aligned(x, 4) ||
+        !aligned(theta, 4) || !aligned(rmse_out, 8))
+        return ALS_ERR_ALIGN;
+    return ALS_OK;
+}
+
+// The RMSE's two kernels on `st`: partials over C = cus * kRmseWavesPerCU fixed chunks (at most
+// cap_per_cu resident waves per CU if positive), then their fixed-order sum.  part holds C
+// doubles; claim is the chunk counter (reset here by a kernel).
+hipError_t rmse_launch(int cus, int cap_per_cu, bool force_global, hipStream_t st,
+                       const int64_t* rowptr, const int32_t* colidx, const float* vals, int64_t m,
+                       int64_t n, int f, const float* x, const float* theta, double* part,
+                       unsigned* claim, double* rmse_out) {
+    const int C = cus * kRmseWavesPerCU;
+    if (m > 0) {
+        const bool buf =
+            !force_global && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
+        hipError_t le = hipSuccess;
+#define ALS_RMSE_ARGS cus, cap_per_cu, st, rowptr, colidx, vals, m, n, f, x, theta, part, claim, C
+        switch (f / 16 + 1) {
+#define ALS_RMSE_CASE(NB)                                                           \
+            case NB:                                                                \
+                le = buf ? rmse_rows_launch<NB, true>(ALS_RMSE_ARGS)                \
+                         : rmse_rows_launch<NB, false>(ALS_RMSE_ARGS);              \
+                break;
+            ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4) ALS_RMSE_CASE(5)
+            ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8) ALS_RMSE_CASE(9)
+#undef ALS_RMSE_CASE
+#undef ALS_RMSE_ARGS
+            default: return hipErrorInvalidValue;
+        }
+        if (le != hipSuccess) return le;
+    }
+    hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? C : 0, part,
+                       rmse_out);
+    return hipGetLastError();
+}
+
 void profile_free(als_ctx* ctx) {
     if (!ctx->prof_ev) return;
     for (int i = 0; i < 4 * ctx->prof_cap; ++i) (void)hipEventDestroy(ctx->prof_ev[i]);
@@ -1926,41 +1974,14 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
              int64_t m, int64_t n, int32_t f, const float* x, const float* theta,
              double* rmse_out, void* stream) {
     if (!ctx) return ALS_ERR_INVALID_ARG;
-    if (f < 1 || f > ALS_F_MAX) return ALS_ERR_UNSUPPORTED_F;
-    if (m < 0 || n < 0 || !rowptr || !rmse_out) return ALS_ERR_INVALID_ARG;
-    if (m > 0 && (!x || (n > 0 && (!colidx || !vals || !theta)))) return ALS_ERR_INVALID_ARG;
-    if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(vals, 4) || !aligned(x, 4) ||
-        !aligned(theta, 4) || !aligned(rmse_out, 8))
-        return ALS_ERR_ALIGN;
+    const int rc = rmse_check(rowptr, colidx, vals, m, n, f, x, theta, rmse_out);
+    if (rc != ALS_OK) return rc;
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
-    hipStream_t st = (hipStream_t)stream;
-    const int C = ctx->cus * kRmseWavesPerCU;
-    double* part = (double*)(ctx->ws + ctx->lay.rmse);
-    auto* claim = (unsigned*)(ctx->ws + ctx->lay.status + 128);
-    hipError_t le = hipSuccess;
-    if (m > 0) {
-        const bool buf =
-            !ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
-#define ALS_RMSE_ARGS ctx->cus, 4 * ctx->rmse_waves_per_simd, st, rowptr, colidx, vals, m, n, f, \
-                      x, theta, part, claim, C
-        switch (f / 16 + 1) {
-#define ALS_RMSE_CASE(NB)                                                           \
-            case NB:                                                                \
-                le = buf ? rmse_rows_launch<NB, true>(ALS_RMSE_ARGS)                \
-                         : rmse_rows_launch<NB, false>(ALS_RMSE_ARGS);              \
-                break;
-            ALS_RMSE_CASE(1) ALS_RMSE_CASE(2) ALS_RMSE_CASE(3) ALS_RMSE_CASE(4) ALS_RMSE_CASE(5)
-            ALS_RMSE_CASE(6) ALS_RMSE_CASE(7) ALS_RMSE_CASE(8) ALS_RMSE_CASE(9)
-#undef ALS_RMSE_CASE
-#undef ALS_RMSE_ARGS
-            default: return ALS_ERR_UNSUPPORTED_F;
-        }
-        if (le != hipSuccess) return fail_hip(ctx, le);
-    }
-    hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(kWave), 0, st, rowptr, m, m > 0 ? C : 0, part,
-                       rmse_out);
-    hipError_t e = hipGetLastError();
+    hipError_t e = rmse_launch(ctx->cus, 4 * ctx->rmse_waves_per_simd, ctx->global_gather,
+                               (hipStream_t)stream, rowptr, colidx, vals, m, n, f, x, theta,
+                               (double*)(ctx->ws + ctx->lay.rmse),
+                               (unsigned*)(ctx->ws + ctx->lay.status + 128), rmse_out);
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
 }
 

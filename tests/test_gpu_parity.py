@@ -227,6 +227,31 @@ def test_not_spd_rows_are_nan_and_counted(ctx):
     assert als.als_status(ctx) == 0
 
 
+def test_overflowing_gram_is_nan_and_counted(ctx):
+    """A Gram matrix that overflows fp32 (theta entries of 1e20: squares of 1e40) has a +inf
+    pivot; the row is NaN and counted, not solved to a finite wrong value."""
+    from paper_1603_03820_amd import als
+    for f in (8, 100):
+        n = 300
+        theta = synthetic_factor(n, f, 23 + f, 0.5)
+        # columns 0..19: every entry at least 1e20, so every product of two overflows fp32
+        theta[:20] = np.float32(1e20) * (1.0 + np.abs(theta[:20]))
+        rng = np.random.default_rng(5)
+        rows = [np.sort(rng.choice(20, 4, replace=False)),           # only overflowing columns
+                np.sort(20 + rng.choice(n - 20, 150, replace=False)),  # generic
+                np.array([3, 40, 41, 200]),                            # one overflowing column
+                np.zeros(0, np.int64)]
+        rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int64)
+        colidx = np.concatenate(rows).astype(np.int32)
+        vals = rng.uniform(1, 5, len(colidx)).astype(np.float32)
+        als.als_status(ctx)   # clear
+        log(f"overflowing Gram f={f}")
+        x = gpu_half_sweep(ctx, rowptr, colidx, vals, 4, n, f, 0.05, theta, sentinel=7.0)
+        assert np.all(np.isnan(x[0])) and np.all(np.isnan(x[2])), f
+        assert np.all(np.isfinite(x[1])) and np.all(x[3] == 0.0), f
+        assert als.als_status(ctx) == 2, f
+
+
 def test_empty_inputs(ctx):
     from paper_1603_03820_amd import als
     dev = ctx.device
