@@ -74,32 +74,57 @@ def parse():
                     help="run each step's RMSE after its update-Theta on the same stream (default: "
                          "on a second stream and context, one wave per SIMD, beside the next "
                          "step's update-X, with X double-buffered)")
+    ap.add_argument("--other-steps", type=int, default=3,
+                    help="timed steps per other workload (rank sweep, music, wiki)")
+    ap.add_argument("--no-others", action="store_true",
+                    help="time the headline workload only (no rank sweep, music or wiki block)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
                          "calibration), then one user and one item half-sweep; no JSON")
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_herm_solve_movie_f100_traffic.txt")
 KERNEL_SRC = os.path.join(ROOT, "paper_1603_03820_amd", "csrc", "als.hip")
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per k_herm_solve launch from the committed counter summary, if it was taken on
-    this workload and on the kernel source as it is now (else None)."""
+def traffic_file(tag: str) -> str:
+    """The committed counter summary of k_herm_solve's HBM traffic on one workload."""
+    return os.path.join(ROOT, "profiles", f"k_herm_solve_{tag}_traffic.txt")
+
+
+def measured_traffic(workload: str, tag: str = "movie_f100", key: str = "bytes_per_launch"):
+    """HBM bytes per k_herm_solve launch (or per user / item launch with key bytes_user_launch,
+    bytes_item_launch) from the committed counter summary, if it was taken on this workload
+    and on the kernel source as it is now (else None)."""
     import hashlib
-    if not os.path.exists(TRAFFIC_FILE):
+    path = traffic_file(tag)
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if (kv.get("source_sha256") != src or kv.get("workload") != workload
-            or "bytes_per_launch" not in kv):
+    if kv.get("source_sha256") != src or kv.get("workload") != workload or key not in kv:
         return None
-    return float(kv["bytes_per_launch"])
+    return float(kv[key])
+
+
+def roofline_bound(flops: float, nbytes: float):
+    """The roofline that bounds a kernel doing `flops` with `nbytes` of HBM traffic:
+    min(FP32 peak, HBM peak x AI) in TFLOP/s, and which side binds."""
+    ai = flops / nbytes
+    hbm_tflops = HBM_PEAK_GBS * ai / 1e3
+    if hbm_tflops < FP32_PEAK_TFLOPS:
+        return "hbm", hbm_tflops, ai
+    return "mfma", FP32_PEAK_TFLOPS, ai
+
+
+def algorithmic_bytes(nnz: int, m: int, n: int, f: int) -> float:
+    """Compulsory HBM bytes of one half-sweep: indices + ratings, row pointers, the gathered
+    factor once, the written factor once (A_u never leaves the chip)."""
+    return 8.0 * nnz + 8.0 * (m + 1) + 4.0 * n * f + 4.0 * m * f
 
 
 def split_rows(bounds: np.ndarray, rowptr: np.ndarray) -> int:
@@ -355,9 +380,12 @@ def stream_bench(args):
 
 
 def ablation_bench(args):
-    """User and item half-sweeps under each design alternative the library can select: the
-    gather (bounded buffer loads vs 64-bit global loads: the analogue of the paper's texture
-    cache ablation) and the last block column (quad form vs 16x16 tiles)."""
+    """User and item half-sweeps under each design alternative the library can select (each a
+    context created under its environment setting): the gather (bounded buffer loads straight
+    into MFMA operands; 64-bit global loads, the analogue of the paper's texture-cache ablation;
+    theta rows staged through LDS, the analogue of its shared-memory staging), the last block
+    column (quad form vs 16x16 tiles), and where A_u accumulates (registers for the whole row vs
+    device memory every 16 ratings, the analogue of the paper's register ablation)."""
     import torch
     import synth
     from paper_1603_03820_amd import als, driver
@@ -371,17 +399,20 @@ def ablation_bench(args):
     theta0 = torch.from_numpy(p.theta0).to(dev)
     x = torch.empty((p.m, f), dtype=torch.float32, device=dev)
     th = torch.empty_like(theta0)
-    variants = [("buffer", "quad"), ("buffer", "tiles"), ("global", "quad"), ("global", "tiles")]
+    variants = [
+        ("buffer", "quad", "registers", {}),
+        ("buffer", "tiles", "registers", {"ALS_LAST_BLOCK": "tiles"}),
+        ("global", "tiles", "registers", {"ALS_GATHER": "global"}),
+        ("lds-staged", "tiles", "registers", {"ALS_GATHER": "lds"}),
+        ("buffer", "quad", "memory every 16 ratings", {"ALS_PART_ENTRIES": "16"}),
+    ]
     rows = []
-    for gather, last in variants:
-        env = {"ALS_GATHER": "global" if gather == "global" else None,
-               "ALS_LAST_BLOCK": "tiles" if last == "tiles" else None}
-        saved = {k: os.environ.get(k) for k in env}
-        for k, v in env.items():
-            if v is None:
-                os.environ.pop(k, None)
-            else:
-                os.environ[k] = v
+    for gather, last, accum, env in variants:
+        keys = ("ALS_GATHER", "ALS_LAST_BLOCK", "ALS_PART_ENTRIES")
+        saved = {k: os.environ.get(k) for k in keys}
+        for k in keys:
+            os.environ.pop(k, None)
+        os.environ.update(env)
         try:
             ctx = als.Context(0, max(f, 16))
         finally:
@@ -401,9 +432,13 @@ def ablation_bench(args):
         torch.cuda.synchronize()
         prof = np.array([sum(pr) for pr in als.als_profile_end(ctx, 2 * args.steps)])
         prof = prof.reshape(-1, 2)
-        rows.append({"gather": gather, "last_block": last,
+        rows.append({"gather": gather, "last_block": last, "accumulation": accum,
+                     "env": env,
                      "user_ms": round(float(np.median(prof[:, 0])), 4),
                      "item_ms": round(float(np.median(prof[:, 1])), 4)})
+        print(f"[bench] ablation {gather}/{last}/{accum}: {rows[-1]}", file=sys.stderr,
+              flush=True)
+        ctx.close()
         del ctx
     base = rows[0]["user_ms"] + rows[0]["item_ms"]
     for r in rows:
@@ -416,6 +451,121 @@ def ablation_bench(args):
                                   f"lambda={p.lam}"},
            "variants": rows}
     print(json.dumps(out), flush=True)
+
+
+def side_figures(ctx, rowptr_dev, rowptr, m, n, nnz, f, plan_ms, herm_ms, red_ms, tag, side,
+                 workload):
+    """Per half-sweep side: median times, k_herm_solve's algorithmic rate against the FP32 peak
+    and against its own roofline (counter traffic if committed for this workload and source,
+    else the compulsory bytes), and the algorithmic Gram / solve split."""
+    from paper_1603_03820_amd import als
+    cnt = np.diff(rowptr)
+    rows = int((cnt > 0).sum())
+    bounds, _ = als.als_plan(ctx, rowptr_dev, m, f)
+    split = split_rows(bounds.cpu().numpy(), rowptr)
+    gram = nnz * F_h(f)
+    herm_fl = gram + (rows - split) * F_s(f)
+    herm = float(np.median(herm_ms))
+    achieved = herm_fl / (herm * 1e-3) / 1e12
+    counted = measured_traffic(workload, tag, f"bytes_{side}_launch")
+    nbytes = counted if counted is not None else algorithmic_bytes(nnz, m, n, f)
+    bound, peak, ai = roofline_bound(herm_fl, nbytes)
+    return {
+        "half_sweep_ms": round(float(np.median(plan_ms + herm_ms + red_ms)), 4),
+        "herm_ms": round(herm, 4), "reduce_ms": round(float(np.median(red_ms)), 4),
+        "herm_tflops": round(achieved, 3), "herm_frac_fp32_peak": round(achieved / FP32_PEAK_TFLOPS, 4),
+        "roofline": {"bound": bound, "peak_tflops": round(peak, 2), "ai_flop_per_byte": round(ai, 2),
+                     "bytes": nbytes, "bytes_source": "counters" if counted is not None
+                     else "algorithmic (no counters for this workload and source)",
+                     "frac": round(achieved / peak, 4)},
+        "flops": {"gram": gram, "solve": rows * F_s(f),
+                  "gram_share": round(gram / (gram + rows * F_s(f)), 4)},
+        "rows": rows, "split_rows": split,
+    }
+
+
+def time_workload(ctx, dp, theta0, steps, warmup, rowptr, colptr, tag, name):
+    """update-X + update-Theta `steps` times (after `warmup`), each half-sweep's three kernels
+    timed by the library's HIP events on the stream they run on; both sides' figures."""
+    import torch
+    from paper_1603_03820_amd import als, driver
+    x = torch.empty((dp.m, dp.f), dtype=torch.float32, device=theta0.device)
+    th = torch.empty_like(theta0)
+    for _ in range(warmup):
+        driver.update_x(ctx, dp, theta0, x)
+        driver.update_theta(ctx, dp, x, th)
+    torch.cuda.synchronize()
+    als.als_profile_begin(ctx, 2 * steps)
+    for _ in range(steps):
+        driver.update_x(ctx, dp, theta0, x)
+        driver.update_theta(ctx, dp, x, th)
+    torch.cuda.synchronize()
+    prof = np.array(als.als_profile_end(ctx, 2 * steps)).reshape(steps, 2, 3)
+    assert als.als_status(ctx) == 0
+    del x, th
+    nnz = int(rowptr[-1])
+    workload = f"{name}: m={dp.m} n={dp.n} nnz={nnz} f={dp.f} lambda={dp.lam}"
+    user = side_figures(ctx, dp.rowptr, rowptr, dp.m, dp.n, nnz, dp.f, prof[:, 0, 0],
+                        prof[:, 0, 1], prof[:, 0, 2], tag, "user", workload)
+    item = side_figures(ctx, dp.colptr, colptr, dp.n, dp.m, nnz, dp.f, prof[:, 1, 0],
+                        prof[:, 1, 1], prof[:, 1, 2], tag, "item", workload)
+    fl = [nnz * F_h(dp.f) + user["rows"] * F_s(dp.f) - user["split_rows"] * F_s(dp.f),
+          nnz * F_h(dp.f) + item["rows"] * F_s(dp.f) - item["split_rows"] * F_s(dp.f)]
+    pair_ms = user["herm_ms"] + item["herm_ms"]
+    pair = (fl[0] + fl[1]) / (pair_ms * 1e-3) / 1e12
+    sweeps_ms = user["half_sweep_ms"] + item["half_sweep_ms"]
+    return {"workload": workload, "steps": steps,
+            "half_sweeps_per_s": round(2e3 / sweeps_ms, 3),
+            "herm_pair_tflops": round(pair, 3),
+            "herm_pair_frac_fp32_peak": round(pair / FP32_PEAK_TFLOPS, 4),
+            "user": user, "item": item}
+
+
+def other_workloads(args, dev, movie):
+    """The other paper-shaped workloads, measured after the headline: the rank sweep on the
+    movie-shaped matrix (f = 32, 64, 128, fresh initial factors), the music shape and the
+    wiki shape (its CSC built on the device), each timed as time_workload does."""
+    import gc
+    import torch
+    import synth
+    from paper_1603_03820_amd import als, driver
+    out = {}
+    p, dp100 = movie
+    for f in synth.RANK_SWEEP_F:
+        t0 = time.perf_counter()
+        dp = driver.DeviceProblem(p.m, p.n, f, p.lam, dp100.rowptr, dp100.colidx, dp100.vals,
+                                  dp100.colptr, dp100.rowidx, dp100.vals_t)
+        th0 = torch.from_numpy(synth.normal(synth.RANK_SWEEP_THETA_SEED, synth.THETA0_STREAM,
+                                            (p.n, f), synth.THETA0_STD)).to(dev)
+        ctx = als.Context(0, max(f, 16))
+        r = time_workload(ctx, dp, th0, args.other_steps, 1, p.rowptr, p.csc()[0],
+                          f"movie_f{f}", p.name)
+        r["wall_s"] = round(time.perf_counter() - t0, 1)
+        out[f"movie_f{f}"] = r
+        print(f"[bench] movie f={f}: {r['half_sweeps_per_s']} half-sweeps/s", file=sys.stderr,
+              flush=True)
+        ctx.close()
+    for name in ("music", "wiki"):
+        t0 = time.perf_counter()
+        q = synth.config(name)
+        ctx = als.Context(0, max(q.f, 16))
+        t = lambda a: torch.from_numpy(a).to(dev)  # noqa: E731
+        rp, ci, v = t(q.rowptr), t(q.colidx), t(q.vals)
+        colptr, rowidx, vt = als.als_csr_to_csc(ctx, rp, ci, v, q.m, q.n, nnz=q.nnz)
+        dp = driver.DeviceProblem(q.m, q.n, q.f, q.lam, rp, ci, v, colptr, rowidx, vt)
+        gen_s = time.perf_counter() - t0
+        r = time_workload(ctx, dp, t(q.theta0), args.other_steps, 1, q.rowptr,
+                          colptr.cpu().numpy(), f"{name}_f{q.f}", q.name)
+        r["wall_s"] = round(time.perf_counter() - t0, 1)
+        r["gen_s"] = round(gen_s, 1)
+        out[name] = r
+        print(f"[bench] {name}: {r['half_sweeps_per_s']} half-sweeps/s", file=sys.stderr,
+              flush=True)
+        ctx.close()
+        del q, rp, ci, v, colptr, rowidx, vt, dp
+        gc.collect()
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -539,13 +689,26 @@ def main():
     herm_avg_fl = float(np.mean(herm_fl))
     achieved = herm_avg_fl / (herm_avg_ms * 1e-3) / 1e12
     workload = f"{p.name}: m={p.m} n={p.n} nnz={nnz} f={f} lambda={p.lam}"
+    traffic = measured_traffic(workload)
+    # the bound: min(FP32 peak, HBM peak x AI), AI from the counter bytes when they were taken
+    # on this workload and kernel source, else from the compulsory bytes
+    ai_bytes = traffic if traffic is not None else float(np.mean(
+        [algorithmic_bytes(nnz, p.m, p.n, f), algorithmic_bytes(nnz, p.n, p.m, f)]))
+    bound, _, ai = roofline_bound(herm_avg_fl, ai_bytes)
+    if bound == "mfma":
+        ach, peak, unit = achieved, FP32_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        ach, peak, unit = ai_bytes / (herm_avg_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"
     roofline = {
         "kernel": f"k_herm_solve<{(f + 15) // 16}> (Gram via fp32 MFMA + in-register Cholesky)",
-        "bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS,
-        "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
-        "traffic": measured_traffic(workload),
+        "bound": bound, "achieved": round(ach, 3), "peak": peak,
+        "unit": unit, "frac": round(ach / peak, 4),
+        "traffic": traffic,
+        "ai_flop_per_byte": round(ai, 2),
+        "ai_bytes": "counters" if traffic is not None else "algorithmic",
         "avg_launch_ms": round(herm_avg_ms, 4),
         "flops_per_launch": herm_avg_fl,
+        "tflops": round(achieved, 3),
     }
 
     out = {
@@ -593,6 +756,12 @@ def main():
             achieved / out["peaks_measured"]["mfma_f32_tflops"], 4)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(p, csc, args.cpu_flops, args.cpu_stride)
+    if not args.no_others and p.name == "movie":
+        torch.cuda.synchronize()
+        try:
+            out["workloads"] = other_workloads(args, dev, (p, dp))
+        except Exception as e:   # the headline line is printed whatever happens here
+            out["workloads_error"] = f"{type(e).__name__}: {e}"
     print(json.dumps(out), flush=True)
 
 

@@ -72,7 +72,12 @@ size_t als_workspace_bytes(int device, int32_t f_max);
      ALS_GATHER=global      gather theta/x with 64-bit global loads at every size (otherwise
                             bounded buffer loads whenever the factor is below 2 GiB);
      ALS_LAST_BLOCK=tiles   accumulate the last block column with 16x16x4 tiles even when its
-                            quad form applies (f = 0 or 4 mod 16). */
+                            quad form applies (f = 0 or 4 mod 16).
+   A third sets the part length of long pieces (tests; the default is 65,536 entries):
+     ALS_PART_ENTRIES=k     a row piece longer than k entries (rounded down to 16 times a power
+                            of two) is accumulated in parts of that length, whose sums are added
+                            in order in a per-wave slot of the workspace (a two-level sum: no
+                            fp32 running sum spans more than one part). */
 int als_init(als_ctx** ctx, int device, void* workspace, size_t workspace_bytes, int32_t f_max);
 
 /* Release the context (not the workspace).  Does not synchronise. */

@@ -284,11 +284,14 @@ __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc
 //     loads are clamped to valid addresses (row 0 past the end, column 0 for padding) and the
 //     values are masked when consumed.
 // Both issue their loads unconditionally, so they stay in flight across earlier matrix ops.
-template <int NB, bool BUF, int P = 0>
+// Gather forms (the second template argument).
+constexpr int kFormGlobal = 0, kFormBuffer = 1, kFormStaged = 2;
+
+template <int NB, int BUF, int P = 0>
 struct Gather;
 
 template <int NB, int P>
-struct Gather<NB, true, P> {
+struct Gather<NB, kFormBuffer, P> {
     static constexpr bool kMasked = false;
     static constexpr int kBuf = NB + (P > 1 ? P - 1 : 0);   // operand values per step
     __amdgpu_buffer_rsrc_t rs;
@@ -297,7 +300,8 @@ struct Gather<NB, true, P> {
     // quad form: quads 0..P-2 hold theta columns 16 (NB-1) + 4p + (lane & 3) (all below f), and
     // quad P-1 holds only the rating, in its first column (f = 16 (NB-1) + 4 (P-1))
     unsigned lw[P > 1 ? P - 1 : 1];
-    __device__ __forceinline__ Gather(const float* theta, int64_t n, int f, int c) {
+    __device__ __forceinline__ Gather(const float* theta, int64_t n, int f, int c,
+                                      float* = nullptr) {
         fbytes = 4u * (unsigned)f;
         size = (unsigned)n * fbytes;
         rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(theta), 0, (int)size,
@@ -341,14 +345,15 @@ struct Gather<NB, true, P> {
 };
 
 template <int NB>
-struct Gather<NB, false, 0> {
+struct Gather<NB, kFormGlobal, 0> {
     static constexpr bool kMasked = true;
     static constexpr int kBuf = NB;
     const float* theta;
     int f;
     int jl[NB];
     bool jv[NB], jr[NB];
-    __device__ __forceinline__ Gather(const float* th, int64_t, int f_, int c) : theta(th), f(f_) {
+    __device__ __forceinline__ Gather(const float* th, int64_t, int f_, int c, float* = nullptr)
+        : theta(th), f(f_) {
 #pragma unroll
         for (int I = 0; I < NB; ++I) {
             const int j = 16 * I + c;
@@ -368,6 +373,65 @@ struct Gather<NB, false, 0> {
         const float rr = ok ? r : 0.f;
 #pragma unroll
         for (int I = 0; I < NB; ++I) v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? rr : 0.f);
+    }
+};
+
+// Gather<NB, kFormStaged>: a design alternative (for the ablation of the gather; theta below
+// 2 GiB, f a multiple of 4): the step's four theta rows are read row by row with two 16-byte
+// loads per lane -- lane (g, c) reads bytes 16 c and 256 + 16 c of row g, the rating lane's
+// bytes included -- written to a per-wave LDS buffer of four rows of 16 NB floats (zero past
+// the loaded columns), and the MFMA operands are read back from it (lane (g, c) of block I:
+// row g, column 16 I + c).  Past the piece's end and past a row's 4 f bytes the loads are out of
+// range and return zeros, as in the buffer form.
+constexpr int stage_floats(int nb) { return 4 * 16 * nb; }
+
+template <int NB>
+struct Gather<NB, kFormStaged, 0> {
+    static constexpr bool kMasked = false;
+    static constexpr int kBuf = 8;
+    __amdgpu_buffer_rsrc_t rs;
+    unsigned fbytes, size, o0, o1;
+    int lane;
+    bool jr;
+    float* stage;
+    __device__ __forceinline__ Gather(const float* theta, int64_t n, int f, int c, float* st) {
+        fbytes = 4u * (unsigned)f;
+        size = (unsigned)n * fbytes;
+        rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(theta), 0, (int)size,
+                                               0x00020000);
+        o0 = 16u * c < fbytes ? 16u * c : size;
+        o1 = 256u + 16u * c < fbytes ? 256u + 16u * c : size;
+        jr = 16 * (NB - 1) + c == f;
+        lane = (int)(threadIdx.x & 63);
+        stage = st;
+    }
+    __device__ __forceinline__ int word(int col, bool valid) const {
+        return valid ? (int)((unsigned)col * fbytes) : (int)size;
+    }
+    __device__ __forceinline__ void issue(int e, float (&v)[kBuf]) const {
+        const f4 a = __builtin_bit_cast(
+            f4, __builtin_amdgcn_raw_buffer_load_b128(rs, (unsigned)e + o0, 0, 0));
+        const f4 b = __builtin_bit_cast(
+            f4, __builtin_amdgcn_raw_buffer_load_b128(rs, (unsigned)e + o1, 0, 0));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[j] = a[j];
+            v[4 + j] = b[j];
+        }
+    }
+    __device__ __forceinline__ void operands(const float (&B)[kBuf], float r, bool,
+                                             float (&v)[NB], float (&)[1]) const {
+        const int g = lane >> 4, c = lane & 15;
+        float* row = stage + g * 16 * NB;
+        if (4 * c + 4 <= 16 * NB)
+            *reinterpret_cast<f4*>(row + 4 * c) = f4{B[0], B[1], B[2], B[3]};
+        if (64 + 4 * c + 4 <= 16 * NB)
+            *reinterpret_cast<f4*>(row + 64 + 4 * c) = f4{B[4], B[5], B[6], B[7]};
+        __syncthreads();
+#pragma unroll
+        for (int I = 0; I < NB; ++I) v[I] = row[16 * I + c];
+        if (jr) v[NB - 1] = r;
+        __syncthreads();   // the next step rewrites the rows
     }
 };
 
@@ -476,6 +540,10 @@ __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restric
     int qb = 0, k = 0;       // group's position in its batch; batch of the group's steps
     int rq = 4 * kDepth;     // ring position of the first step issued in the group
     for (int q = 0; q < ngroups; ++q) {
+        if constexpr (Body::kParts) {
+            // at every part boundary the body folds its accumulators away (see GramBody)
+            if (q > 0 && (q & body.part_mask) == 0) body.flush(q == body.part_mask + 1);
+        }
         // batch k+1 goes into the ring at the top of group 1, one group after its load was
         // issued at the top of group 0 (the store comes first in program order, so its wait
         // never covers the gathers issued after the load)
@@ -496,13 +564,103 @@ __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restric
     __syncthreads();   // the ring is refilled by the next piece
 }
 
+// A piece longer than a part (kPart entries by default; a power of two times the 16 entries of a
+// pipeline group) runs in parts (the last one shorter): each part's Gram is accumulated in
+// registers from zero, and the parts' sums are added in order into the wave's own
+// partial-accumulator slot in the workspace, the second level of a two-level sum, so that no fp32
+// running sum spans more than a part (a column of tens of millions of ratings otherwise
+// accumulates over a million entries in one register chain).  After the last part the slot is
+// added into the registers and the piece goes on as one accumulator.
+constexpr int64_t kPart = 1 << 16;
+constexpr int kEntriesPerGroup = 4 * kGroup;
+
+// A partial-accumulator slot: tile t of lane l at f4 index 64 t + l (16 contiguous bytes per
+// lane, 1 KiB per tile).
+template <int NB>
+__device__ __forceinline__ void store_slot(const f4 (&acc)[ntiles(NB)], float* __restrict__ slot,
+                                           int lane) {
+    f4* s = reinterpret_cast<f4*>(slot);
+#pragma unroll
+    for (int t = 0; t < ntiles(NB); ++t) s[t * kWave + lane] = acc[t];
+}
+
+// acc += slot.  All loads are issued before the first add (a dependent load-add chain would
+// leave one load in flight at a time).
+template <int NB>
+__device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], const float* __restrict__ slot,
+                                         int lane) {
+    const f4* s = reinterpret_cast<const f4*>(slot);
+    f4 v[ntiles(NB)];
+#pragma unroll
+    for (int t = 0; t < ntiles(NB); ++t) v[t] = s[t * kWave + lane];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < ntiles(NB); ++t) acc[t] += v[t];
+}
+
+// slot += acc, four tiles at a time (the temporaries stay at 16 registers beside the
+// accumulators).
+template <int NB>
+__device__ __forceinline__ void fold_into_slot(const f4 (&acc)[ntiles(NB)],
+                                               float* __restrict__ slot, int lane) {
+    f4* s = reinterpret_cast<f4*>(slot);
+#pragma unroll
+    for (int t0 = 0; t0 < ntiles(NB); t0 += 4) {
+        f4 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (t0 + j < ntiles(NB)) v[j] = s[(t0 + j) * kWave + lane];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (t0 + j < ntiles(NB)) s[(t0 + j) * kWave + lane] = v[j] + acc[t0 + j];
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// acc += slot, four tiles at a time.
+template <int NB>
+__device__ __forceinline__ void add_slot_in_fours(f4 (&acc)[ntiles(NB)],
+                                                  const float* __restrict__ slot, int lane) {
+    const f4* s = reinterpret_cast<const f4*>(slot);
+#pragma unroll
+    for (int t0 = 0; t0 < ntiles(NB); t0 += 4) {
+        f4 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (t0 + j < ntiles(NB)) v[j] = s[(t0 + j) * kWave + lane];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (t0 + j < ntiles(NB)) acc[t0 + j] += v[j];
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // The Gram body: accumulate the upper block-triangle of the augmented Gram matrix into acc
-// (and the quad accumulators of the last block column).
-template <int NB, int P, class G>
+// (and the quad accumulators of the last block column).  Every kPartGroups groups the pipeline
+// calls flush(): the accumulators so far (the quad ones turned into tiles) are stored into, or
+// added to, the wave's slot, and start again from zero.
+template <int NB, int P>
+__device__ __forceinline__ void zero_quads(QuadAcc<NB, P>& qa) {
+    if constexpr (P > 0) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+#pragma unroll
+            for (int p = 0; p + 1 < P; ++p) qa.q[I][p] = f4{0.f, 0.f, 0.f, 0.f};
+            qa.b[I] = 0.f;
+        }
+    }
+}
+
+template <int NB, int P, class G, bool PARTS>
 struct GramBody {
+    static constexpr bool kParts = PARTS;
+    int part_mask;        // groups per part - 1 (a power of two - 1)
     const G& gat;
     f4 (&acc)[ntiles(NB)];
     QuadAcc<NB, P>& qa;
+    void* quad_scratch;   // LDS for the quad exchange
+    float* wslot;         // the wave's slot
+    int lane;
     float v[NB], w[P > 0 ? P : 1], r;
     __device__ __forceinline__ void take(const float (&B)[G::kBuf], float rr, bool ok) {
         gat.operands(B, rr, ok, v, w);
@@ -510,15 +668,25 @@ struct GramBody {
     }
     template <int J>
     __device__ __forceinline__ void run() { mfma_step<NB, P>(v, w, r, acc, qa); }
+    __device__ __forceinline__ void flush(bool first) {
+        if constexpr (P > 0) quad_to_tiles<NB, P>(qa, acc, quad_scratch, lane);
+        if (first) store_slot<NB>(acc, wslot, lane);
+        else fold_into_slot<NB>(acc, wslot, lane);
+#pragma unroll
+        for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+        zero_quads<NB, P>(qa);
+    }
 };
 
-template <int NB, int P, class G>
+template <int NB, int P, bool PARTS, class G>
 __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
                                           int64_t kend, f4 (&acc)[ntiles(NB)],
                                           QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
-                                          Inflight<G::kBuf>& in) {
-    GramBody<NB, P, G> body{gat, acc, qa, {}, {}, 0.f};
+                                          Inflight<G::kBuf>& in, void* quad_scratch,
+                                          float* wslot, int part_mask) {
+    GramBody<NB, P, G, PARTS> body{part_mask, gat, acc, qa, quad_scratch, wslot, lane, {}, {},
+                                   0.f};
     pipe_loop(gat, colidx, vals, kbeg, kend, ring, lane, in, body);
 }
 
@@ -533,6 +701,7 @@ constexpr int dump_floats() { return 16 * (NB + 3); }
 
 template <int NB, int P, class G>
 struct DumpBody {
+    static constexpr bool kParts = false;
     const G& gat;
     float* __restrict__ out;
     int64_t limit;   // entries that fit in out
@@ -560,15 +729,20 @@ struct DumpBody {
     }
 };
 
-template <int NB, bool BUF, int P>
+template <int NB, int BUF, int P>
 __global__ __launch_bounds__(kWave) void k_gather_dump(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t n, int f, int64_t u,
     float* __restrict__ out, int64_t limit) {
     using G = Gather<NB, BUF, P>;
     __shared__ RingEntry ring[kRing];
+    __shared__ __attribute__((aligned(16))) float stage[BUF == kFormStaged ? stage_floats(NB) : 4];
     const int lane = threadIdx.x;
-    const G gat(theta, n, f, lane & 15);
+    if constexpr (BUF == kFormStaged) {
+        for (int i = lane; i < stage_floats(NB); i += kWave) stage[i] = 0.f;
+        __syncthreads();
+    }
+    const G gat(theta, n, f, lane & 15, stage);
     const int64_t kbeg = rowptr[u], kend = rowptr[u + 1];
     RowIndex ix;
     Inflight<G::kBuf> in;
@@ -895,30 +1069,6 @@ __device__ __forceinline__ void write_zero_row(float* __restrict__ xrow, int f, 
     for (int j = lane; j < f; j += kWave) xrow[j] = 0.f;
 }
 
-// A partial-accumulator slot: tile t of lane l at f4 index 64 t + l (16 contiguous bytes per
-// lane, 1 KiB per tile).
-template <int NB>
-__device__ __forceinline__ void store_slot(const f4 (&acc)[ntiles(NB)], float* __restrict__ slot,
-                                           int lane) {
-    f4* s = reinterpret_cast<f4*>(slot);
-#pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t) s[t * kWave + lane] = acc[t];
-}
-
-// acc += slot.  All loads are issued before the first add (a dependent load-add chain would
-// leave one load in flight at a time).
-template <int NB>
-__device__ __forceinline__ void add_slot(f4 (&acc)[ntiles(NB)], const float* __restrict__ slot,
-                                         int lane) {
-    const f4* s = reinterpret_cast<const f4*>(slot);
-    f4 v[ntiles(NB)];
-#pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t) v[t] = s[t * kWave + lane];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int t = 0; t < ntiles(NB); ++t) acc[t] += v[t];
-}
-
 // ------------------------------------------------------------------------ kernels --------
 
 // Persistent waves claim chunks in order from a counter; chunk c covers the entries from
@@ -932,18 +1082,34 @@ struct Piece {
     bool whole;            // the chunk holds the whole row
 };
 
-template <int NB, bool BUF, int P>
+template <int NB, int BUF, int P, bool PARTS>
 __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(NB <= 8 ? 2 : 1)))
 void k_herm_solve(
     const int64_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t m, int64_t n,
     int f, float lambda, int C, const int64_t* __restrict__ bounds, float* __restrict__ x_out,
-    float* __restrict__ slots, unsigned long long* __restrict__ nonspd,
-    unsigned* __restrict__ chunk_ctr) {
+    float* __restrict__ slots, float* __restrict__ wave_slots, int part_mask, int64_t c_row,
+    unsigned long long* __restrict__ nonspd, unsigned* __restrict__ chunk_ctr) {
+    // Both instantiations (with and without parts) are launched; the one that does not match
+    // this call returns at once.  A piece lies within a chunk and within a row: a chunk holds at
+    // most ceil(T1 / W) cost units (c_nnz per entry) plus the snapping of its two cut offsets,
+    // and a row at most n entries (its columns are distinct).
+    {
+        const int64_t T = kCostPerEntry * rowptr[m] + c_row * m;
+        int64_t longest = (T / (int64_t)gridDim.x + 1) / kCostPerEntry + 2 * kSnap + 1;
+        if (longest > n) longest = n;
+        if ((longest > (int64_t)kEntriesPerGroup * (part_mask + 1)) != PARTS) return;
+    }
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
     __shared__ RingEntry ring[kRing];
+    __shared__ __attribute__((aligned(16))) float stage[BUF == kFormStaged ? stage_floats(NB) : 4];
     const int lane = threadIdx.x;
-    const Gather<NB, BUF, P> gat(theta, n, f, lane & 15);
+    if constexpr (BUF == kFormStaged) {
+        for (int i = lane; i < stage_floats(NB); i += kWave) stage[i] = 0.f;
+        __syncthreads();
+    }
+    const Gather<NB, BUF, P> gat(theta, n, f, lane & 15, stage);
+    float* __restrict__ wslot = wave_slots + (size_t)blockIdx.x * slot_floats(NB);
     // No lane-0-only region in the claim loop: every lane takes part in the claim (lane 0 adds
     // one, the others zero), and the wave's count of non-SPD rows stays in a register until the
     // loop has ended (a lane-0 region at each end of a loop body can be joined across the back
@@ -989,20 +1155,19 @@ void k_herm_solve(
 #pragma unroll
             for (int t = 0; t < ntiles(NB); ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
             QuadAcc<NB, P> qa;
-            if constexpr (P > 0) {
-#pragma unroll
-                for (int I = 0; I < NB; ++I) {
-#pragma unroll
-                    for (int p = 0; p + 1 < P; ++p) qa.q[I][p] = f4{0.f, 0.f, 0.f, 0.f};
-                    qa.b[I] = 0.f;
-                }
-            }
-            gram_loop<NB, P>(gat, colidx, vals, cur.beg, cur.end, acc, qa, ring, lane, in);
+            zero_quads<NB, P>(qa);
+            gram_loop<NB, P, PARTS>(gat, colidx, vals, cur.beg, cur.end, acc, qa, ring, lane,
+                                    in, &lds, wslot, part_mask);
             if (more) gram_stage(gat, ix, ring, lane, in);
             if constexpr (P > 0) {
                 static_assert(quad_scratch_bytes<NB, P>() <= sizeof(SolveLds<NB>),
                               "the quad exchange reuses the solve's LDS");
                 quad_to_tiles<NB, P>(qa, acc, &lds, lane);
+            }
+            // a piece longer than a part: its earlier parts' sum is in the wave's slot
+            if constexpr (PARTS) {
+                if (cur.end - cur.beg > (int64_t)kEntriesPerGroup * (part_mask + 1))
+                    add_slot_in_fours<NB>(acc, wslot, lane);
             }
             // the solve is a latency-bound chain; raised priority lets it win issue slots over
             // the other wave's independent Gram MFMAs, which then fill the solve's gaps
@@ -1172,6 +1337,7 @@ __global__ __launch_bounds__(kWave) void k_reduce_solve(
 // rating that the gather puts in column f).
 template <int NB, class G>
 struct RmseBody {
+    static constexpr bool kParts = false;
     const G& gat;
     const float (&xr)[NB];
     double& acc;
@@ -1533,21 +1699,24 @@ __global__ __launch_bounds__(kWave) void k_tr_scatter(
 // --------------------------------------------------------------------- host side ---------
 
 struct Layout {
-    size_t status, bounds, rmse, slots, total;
+    size_t status, bounds, rmse, slots, wave_slots, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // waves[nb] = W for f in (16 (nb-1), 16 nb]; the slot region holds 2 C partial accumulators,
-// C = chunks_of(W)
+// C = chunks_of(W), and the wave-slot region one more per wave (the second summation level of
+// long pieces)
 Layout make_layout(const int* waves, int nb_max, int cus) {
     int c_cap = 1;
-    size_t slot_bytes = 0;
+    size_t slot_bytes = 0, wave_bytes = 0;
     for (int nb = 1; nb <= nb_max; ++nb) {
         const int C = chunks_of(waves[nb]);
         if (C > c_cap) c_cap = C;
         const size_t sb = sizeof(float) * (size_t)slot_floats(nb) * 2 * (size_t)C;
         if (sb > slot_bytes) slot_bytes = sb;
+        const size_t wb = sizeof(float) * (size_t)slot_floats(nb) * (size_t)waves[nb];
+        if (wb > wave_bytes) wave_bytes = wb;
     }
     Layout L;
     size_t off = 0;
@@ -1555,6 +1724,7 @@ Layout make_layout(const int* waves, int nb_max, int cus) {
     L.bounds = off; off = align256(off + sizeof(int64_t) * 2 * (size_t)(c_cap + 1));
     L.rmse = off;   off = align256(off + sizeof(double) * (size_t)cus * kRmseWavesPerCU);
     L.slots = off;  off = align256(off + slot_bytes);
+    L.wave_slots = off; off = align256(off + wave_bytes);
     L.total = off;
     return L;
 }
@@ -1564,11 +1734,18 @@ Layout make_layout(const int* waves, int nb_max, int cus) {
 template <int NB>
 int occupancy_waves(int cus, int* waves) {
     int blocks = 1 << 30;
-    const void* forms[] = {(const void*)k_herm_solve<NB, true, 0>,
-                           (const void*)k_herm_solve<NB, true, 1>,
-                           kQuad2<NB> ? (const void*)k_herm_solve<NB, true, kQuad2<NB> ? 2 : 1>
+    const void* forms[] = {(const void*)k_herm_solve<NB, kFormBuffer, 0, false>,
+                           (const void*)k_herm_solve<NB, kFormBuffer, 1, false>,
+                           kQuad2<NB> ? (const void*)k_herm_solve<NB, kFormBuffer,
+                                                                  kQuad2<NB> ? 2 : 1, false>
                                       : nullptr,
-                           (const void*)k_herm_solve<NB, false, 0>};
+                           (const void*)k_herm_solve<NB, kFormGlobal, 0, false>,
+                           (const void*)k_herm_solve<NB, kFormBuffer, 0, true>,
+                           (const void*)k_herm_solve<NB, kFormBuffer, 1, true>,
+                           kQuad2<NB> ? (const void*)k_herm_solve<NB, kFormBuffer,
+                                                                  kQuad2<NB> ? 2 : 1, true>
+                                      : nullptr,
+                           (const void*)k_herm_solve<NB, kFormGlobal, 0, true>};
     for (const void* k : forms) {
         if (!k) continue;
         int b = 0;
@@ -1618,6 +1795,38 @@ int waves_for_nb(int nb, int cus, int* w) {
     }
 }
 
+template <int NB>
+int staged_occupancy(int cus, int* waves) {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &b, (const void*)k_herm_solve<NB, kFormStaged, 0, true>, kWave, 0) != hipSuccess)
+        return -1;
+    int b2 = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &b2, (const void*)k_herm_solve<NB, kFormStaged, 0, false>, kWave, 0) != hipSuccess)
+        return -1;
+    if (b2 < b) b = b2;
+    if (b < 1) b = 1;
+    if (b > kMaxWavesPerCU) b = kMaxWavesPerCU;
+    *waves = b * cus;
+    return 0;
+}
+
+int staged_waves_for_nb(int nb, int cus, int* w) {
+    switch (nb) {
+        case 1: return staged_occupancy<1>(cus, w);
+        case 2: return staged_occupancy<2>(cus, w);
+        case 3: return staged_occupancy<3>(cus, w);
+        case 4: return staged_occupancy<4>(cus, w);
+        case 5: return staged_occupancy<5>(cus, w);
+        case 6: return staged_occupancy<6>(cus, w);
+        case 7: return staged_occupancy<7>(cus, w);
+        case 8: return staged_occupancy<8>(cus, w);
+        case 9: return staged_occupancy<9>(cus, w);
+        default: return -1;
+    }
+}
+
 int nb_of(int f) { return f / 16 + 1; }   // blocks of 16 covering the augmented f + 1
 
 // Solve cost of one row in c_nnz units: per 16-column block about 2,500 cycles of factor and
@@ -1656,8 +1865,10 @@ struct als_ctx {
     int prof_cap;
     int prof_count;
     bool global_gather;    // use the 64-bit-load gather for every size (ALS_GATHER=global)
+    bool staged_gather;    // stage theta through LDS (ALS_GATHER=lds; ablation)
     bool tile_last_block;  // 16x16 tiles for the last block column always (ALS_LAST_BLOCK=tiles)
     int rmse_waves_per_simd;   // cap on resident RMSE waves per SIMD (0 = as many as fit)
+    int part_groups;           // pipeline groups per part of a long piece (a power of two)
     size_t lds_per_block;      // the device's LDS bytes per workgroup
 };
 
@@ -1704,12 +1915,53 @@ int query_device(int device, int f_max, int* cus, int* waves, int* w_cap,
 // lane's offset, must stay below 2^32
 constexpr uint64_t kBufferGatherMax = 0x7FFFF000ull;
 
+// The staged gather (an ablation form) reads whole 16-byte groups of a row through one buffer
+// descriptor.
+bool staged_supported(int64_t n, int f) {
+    return f % 4 == 0 && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax;
+}
+
+struct HermArgs {
+    const int64_t* rowptr;
+    const int32_t* colidx;
+    const float* vals;
+    const float* theta;
+    int64_t m, n;
+    int f;
+    float lambda;
+    int C;
+    const int64_t* bounds;
+    float* x;
+    float* slots;
+    float* wslots;
+    int part_mask;
+    int64_t c_row;
+    unsigned long long* nonspd;
+    unsigned* chunk_ctr;
+};
+
+// Both instantiations; the kernels pick the one that runs from rowptr[m] on the device (no
+// host synchronisation), the other returns at once.
+template <int NB, int BUF, int P>
+void launch_herm(int W, hipStream_t st, const HermArgs& a) {
+    hipLaunchKernelGGL((k_herm_solve<NB, BUF, P, false>), dim3(W), dim3(kWave), 0, st,
+                       a.rowptr, a.colidx, a.vals, a.theta, a.m, a.n, a.f, a.lambda, a.C,
+                       a.bounds, a.x, a.slots, a.wslots, a.part_mask, a.c_row, a.nonspd,
+                       a.chunk_ctr);
+    hipLaunchKernelGGL((k_herm_solve<NB, BUF, P, true>), dim3(W), dim3(kWave), 0, st,
+                       a.rowptr, a.colidx, a.vals, a.theta, a.m, a.n, a.f, a.lambda, a.C,
+                       a.bounds, a.x, a.slots, a.wslots, a.part_mask, a.c_row, a.nonspd,
+                       a.chunk_ctr);
+}
+
 template <int NB>
 void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const float* vals,
                   int64_t m, int64_t n, int f, float lambda, const float* theta, float* x,
                   hipStream_t st, int W) {
     int64_t* bounds = (int64_t*)(ctx->ws + ctx->lay.bounds);
     float* slots = (float*)(ctx->ws + ctx->lay.slots);
+    float* wslots = (float*)(ctx->ws + ctx->lay.wave_slots);
+    const int part_mask = ctx->part_groups - 1;
     auto* nonspd = (unsigned long long*)(ctx->ws + ctx->lay.status);
     auto* chunk_ctr = (unsigned*)(ctx->ws + ctx->lay.status + 64);
     const int C = chunks_of(W);
@@ -1724,25 +1976,21 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
     const int f_last = f - 16 * (NB - 1);
     const int quads =
         (!ctx->tile_last_block && (f_last == 0 || f_last == 4)) ? f_last / 4 + 1 : 0;
-    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
-        if (quads == 1)
-            hipLaunchKernelGGL((k_herm_solve<NB, true, 1>), dim3(W), dim3(kWave), 0, st, rowptr,
-                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
-                               chunk_ctr);
-        else if (quads == 2) {
-            if constexpr (kQuad2<NB>)
-                hipLaunchKernelGGL((k_herm_solve<NB, true, 2>), dim3(W), dim3(kWave), 0, st,
-                                   rowptr, colidx, vals, theta, m, n, f, lambda, C, bounds, x,
-                                   slots, nonspd, chunk_ctr);
+    const HermArgs a{rowptr, colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, wslots,
+                     part_mask, row_cost(f), nonspd, chunk_ctr};
+    if (ctx->staged_gather) {   // f % 4 == 0 and theta below 2 GiB (checked by the caller)
+        launch_herm<NB, kFormStaged, 0>(W, st, a);
+    } else if (!ctx->global_gather &&
+               (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
+        if (quads == 1) {
+            launch_herm<NB, kFormBuffer, 1>(W, st, a);
+        } else if (quads == 2) {
+            if constexpr (kQuad2<NB>) launch_herm<NB, kFormBuffer, 2>(W, st, a);
+        } else {
+            launch_herm<NB, kFormBuffer, 0>(W, st, a);
         }
-        else
-            hipLaunchKernelGGL((k_herm_solve<NB, true, 0>), dim3(W), dim3(kWave), 0, st, rowptr,
-                               colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
-                               chunk_ctr);
     } else {
-        hipLaunchKernelGGL((k_herm_solve<NB, false, 0>), dim3(W), dim3(kWave), 0, st, rowptr,
-                           colidx, vals, theta, m, n, f, lambda, C, bounds, x, slots, nonspd,
-                           chunk_ctr);
+        launch_herm<NB, kFormGlobal, 0>(W, st, a);
     }
     if (ev) (void)hipEventRecord(ev[2], st);
     if (C > 1) {
@@ -1764,7 +2012,11 @@ void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, con
     const int f_last = f - 16 * (NB - 1);
     const int quads =
         (!ctx->tile_last_block && (f_last == 0 || f_last == 4)) ? f_last / 4 + 1 : 0;
-    if (!ctx->global_gather && (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
+    if (ctx->staged_gather) {
+        hipLaunchKernelGGL((k_gather_dump<NB, kFormStaged, 0>), dim3(1), dim3(kWave), 0, st,
+                           rowptr, colidx, vals, theta, n, f, u, out, limit);
+    } else if (!ctx->global_gather &&
+               (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
         if (quads == 1)
             hipLaunchKernelGGL((k_gather_dump<NB, true, 1>), dim3(1), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, n, f, u, out, limit);
@@ -1859,10 +2111,27 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
     {
         const char* g = getenv("ALS_GATHER");
         ctx->global_gather = g && strcmp(g, "global") == 0;
+        ctx->staged_gather = g && strcmp(g, "lds") == 0;
         const char* t = getenv("ALS_LAST_BLOCK");
         ctx->tile_last_block = t && strcmp(t, "tiles") == 0;
+        // part length in entries: kPart, or ALS_PART_ENTRIES rounded down to a power of two
+        // times the entries of a pipeline group (at least one group)
+        int64_t part = kPart;
+        const char* pe = getenv("ALS_PART_ENTRIES");
+        if (pe && atoll(pe) > 0) part = atoll(pe);
+        int groups = 1;
+        while ((int64_t)kEntriesPerGroup * groups * 2 <= part && groups < (1 << 24)) groups *= 2;
+        ctx->part_groups = groups;
     }
     ctx->nb_max = nb_of(f_max);
+    if (ctx->staged_gather) {   // the staged form's residency bounds the partition's W
+        DeviceGuard g2(device);
+        for (int nb = 1; nb <= ctx->nb_max; ++nb) {
+            int w = 0;
+            if (staged_waves_for_nb(nb, ctx->cus, &w) != 0) { delete ctx; return ALS_ERR_HIP; }
+            if (w < ctx->waves[nb]) ctx->waves[nb] = w;
+        }
+    }
     ctx->lay = make_layout(ctx->waves, ctx->nb_max, ctx->cus);
     if (workspace_bytes < ctx->lay.total) { delete ctx; return ALS_ERR_WORKSPACE; }
     ctx->ws = (unsigned char*)workspace;
@@ -1949,6 +2218,7 @@ int als_half_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, c
         const char* x1 = x0 + sizeof(float) * (size_t)m * (size_t)f;
         if (t0 < x1 && x0 < t1) return ALS_ERR_ALIAS;
     }
+    if (ctx->staged_gather && !staged_supported(n, f)) return ALS_ERR_UNSUPPORTED_F;
     const int nb = nb_of(f);
     const int W = ctx->waves[nb];
     DeviceGuard guard(ctx->device);
@@ -2107,6 +2377,7 @@ int als_gather_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx,
     if (!aligned(rowptr, 8) || !aligned(colidx, 4) || !aligned(vals, 4) || !aligned(theta, 4) ||
         !aligned(out, 4))
         return ALS_ERR_ALIGN;
+    if (ctx->staged_gather && !staged_supported(n, f)) return ALS_ERR_UNSUPPORTED_F;
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return ALS_ERR_DEVICE;
     hipStream_t st = (hipStream_t)stream;

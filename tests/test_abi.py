@@ -166,7 +166,7 @@ def test_bench_traffic_is_tied_to_workload_and_source():
     bench = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(bench)
     kv = {}
-    for line in open(bench.TRAFFIC_FILE):
+    for line in open(bench.traffic_file("movie_f100")):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
@@ -177,3 +177,4 @@ def test_bench_traffic_is_tied_to_workload_and_source():
     assert bench.measured_traffic(workload) == expect
     assert bench.measured_traffic(workload.replace("f=100", "f=32")) is None
     assert bench.measured_traffic(workload.replace("movie", "music")) is None
+    assert bench.measured_traffic(workload, tag="music_f100") is None

@@ -4,11 +4,11 @@ on the training RMSE over every stored entry.
 
 Rows sampled per side: the longest rows (the heaviest Grams, cut into the most chunk pieces),
 random rows and empty rows.  Item-side inputs and RMSE factors are synthetic factors from the
-generator, never GPU output.  The wiki shape runs at a tenth of its rows here (same row-length
-law, column law and n); ALS_FULL_WIKI=1 runs it at 50M x 40,000 with 3.1B ratings.
+generator, never GPU output.  The wiki shape runs at its full size, 50M x 40,000 with 3.1B
+ratings: it alone has more than 2^31 entries (64-bit entry offsets, the device transpose's
+column-relative positions) and an item-side factor X of 20 GB, past the 2 GiB range of one
+buffer descriptor.
 """
-import os
-
 import numpy as np
 import pytest
 import torch
@@ -46,9 +46,10 @@ def sample_rows(rowptr, k_random, k_long, seed):
 class Side:
     """One side of a workload: host CSR arrays and their device copies."""
 
-    def __init__(self, rowptr, colidx, vals, m, n, dev):
+    def __init__(self, rowptr, colidx, vals, m, n, dev, d=None):
         self.rowptr, self.colidx, self.vals, self.m, self.n = rowptr, colidx, vals, m, n
-        self.d = (to_dev(rowptr, dev), to_dev(colidx, dev), to_dev(vals, dev))
+        self.d = d if d is not None else (to_dev(rowptr, dev), to_dev(colidx, dev),
+                                          to_dev(vals, dev))
 
 
 def check_side(ctx, orc, side, f, lam, theta, label, k_random=600, k_long=8, seed=1):
@@ -146,17 +147,55 @@ def test_music_full_size(ctx, orc):
     check_side(ctx, orc, item, p.f, p.lam, xin, "music item", seed=32)
 
 
-def test_wiki_shape(ctx, orc):
-    scale = 1 if os.environ.get("ALS_FULL_WIKI") == "1" else 10
-    p = load("wiki", m_scale=scale)
-    user = Side(p.rowptr, p.colidx, p.vals, p.m, p.n, ctx.device)
-    check_side(ctx, orc, user, p.f, p.lam, p.theta0, f"wiki/{scale} user", seed=41)
+def test_wiki_full_size(ctx, orc):
+    """Hugewiki-shaped (Table 5), full size: user side, the device transpose at 3.1B entries
+    (bit-exact against the host transpose), item side (the 20 GB X gathered), and the RMSE
+    summed over the CSC so that it gathers from the 20 GB factor too."""
+    from paper_1603_03820_amd import als
+    p = load("wiki")
+    dev = ctx.device
+    user = Side(p.rowptr, p.colidx, p.vals, p.m, p.n, dev)
+    check_side(ctx, orc, user, p.f, p.lam, p.theta0, "wiki user", seed=41)
+    log("wiki: device transpose of 3.1B entries")
     colptr, rowidx, vt = p.csc()
+    dcsc = als.als_csr_to_csc(ctx, *user.d, p.m, p.n, nnz=p.nnz)
+    torch.cuda.synchronize()
+    same = (np.array_equal(dcsc[0].cpu().numpy(), colptr)
+            and torch.equal(dcsc[1], to_dev(rowidx, dev))
+            and torch.equal(dcsc[2].view(torch.int32), to_dev(vt.view(np.int32), dev)))
+    log(f"wiki: device CSC equals the host transpose: {same}")
+    assert same
     del user
-    item = Side(colptr, rowidx, vt, p.n, p.m, ctx.device)
+    item = Side(colptr, rowidx, vt, p.n, p.m, dev, d=dcsc)
     xin = synth.normal(p.recipe["seed"], 8, (p.m, p.f), 0.3)
-    # at full size the longest item rows hold up to 45M ratings, minutes each for the oracle (it
-    # gathers from a 40 GB fp64 factor): sample random rows there; a tenth of the rows keeps
-    # the longest rows in the check
-    check_side(ctx, orc, item, p.f, p.lam, xin, f"wiki/{scale} item", k_random=200,
-               k_long=8 if scale > 1 else 0, seed=42)
+    # at full size the longest item rows hold up to 45M ratings, a minute or more each for the
+    # oracle (it gathers from a 40 GB fp64 factor): the longest row and random rows
+    check_side(ctx, orc, item, p.f, p.lam, xin, "wiki item", k_random=200, k_long=1, seed=42)
+    th = synth.normal(p.recipe["seed"] + 1, 8, (p.n, p.f), 0.3)
+    check_rmse_columns(ctx, orc, colptr, rowidx, vt, p.m, p.f, th, xin, seed=43,
+                       label="wiki (columns, gathering from the 20 GB X)")
+
+
+def check_rmse_columns(ctx, orc, colptr, rowidx, vt, m, f, th, xin, seed, label, k=60):
+    """The RMSE over the ratings of k random columns, computed from the CSC side so that the
+    GPU gathers x_u from the full m x f factor (row indices unchanged); the oracle sums the same
+    entries with the rows renumbered onto the distinct rows they touch (the same terms)."""
+    from paper_1603_03820_amd import als
+    dev = ctx.device
+    rng = np.random.default_rng(seed)
+    cols = np.sort(rng.choice(len(colptr) - 1, size=k, replace=False))
+    lens = colptr[cols + 1] - colptr[cols]
+    sub_ptr = np.zeros(k + 1, np.int64)
+    np.cumsum(lens, out=sub_ptr[1:])
+    idx = np.concatenate([np.arange(colptr[c], colptr[c + 1]) for c in cols])
+    sub_rows, sub_vals = rowidx[idx], vt[idx]
+    log(f"{label}: rmse over {int(sub_ptr[-1])} entries of {k} columns")
+    xd = to_dev(xin, dev)
+    got = float(als.als_rmse(ctx, to_dev(sub_ptr, dev), to_dev(sub_rows, dev),
+                             to_dev(sub_vals, dev), k, m, f, to_dev(th[cols], dev), xd).item())
+    del xd
+    uniq, inv = np.unique(sub_rows, return_inverse=True)
+    ref = orc.rmse(sub_ptr, inv.astype(np.int32), sub_vals, k, f, th[cols].astype(np.float64),
+                   xin[uniq].astype(np.float64))
+    log(f"{label}: rmse gpu {got:.9f} oracle {ref:.9f}")
+    assert abs(got - ref) <= 1e-6 * max(1.0, ref)

@@ -152,6 +152,117 @@ def test_global_gather_form(ctx_global, orc, f):
                    f"global gather edge lengths f={f}")
 
 
+def _env_ctx(**env):
+    import os
+    from paper_1603_03820_amd import als
+    saved = {k: os.environ.get(k) for k in env}
+    os.environ.update({k: str(v) for k, v in env.items()})
+    try:
+        return als.Context(0, 128)
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                del os.environ[k]
+            else:
+                os.environ[k] = v
+
+
+@pytest.mark.parametrize("form", ["buffer", "global", "tiles"])
+@pytest.mark.parametrize("f", [7, 16, 100, 128])
+def test_long_pieces_run_in_parts(orc, f, form):
+    """Parts of 32 entries (the default is 65,536): every row and row piece longer than that is
+    accumulated part by part and the part sums are added in the wave's slot (the two-level sum
+    of a long piece).  Lockstep against the oracle on both sides, in every gather and last-block
+    form."""
+    env = {"ALS_PART_ENTRIES": 32}
+    if form == "global":
+        env["ALS_GATHER"] = "global"
+    if form == "tiles":
+        env["ALS_LAST_BLOCK"] = "tiles"
+    c = _env_ctx(**env)
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=781)
+    check_lockstep(c, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"parts of 32 ({form}) f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 782, 1.0 / np.sqrt(f))
+    check_lockstep(c, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"parts of 32 ({form}) f={f} item")
+    lengths = [0, 1, 31, 32, 33, 47, 48, 49, 63, 64, 65, 1000, 4097, 0, 20_000]
+    rowptr, colidx, vals = _handmade(lengths, 30_000, seed=f + 9)
+    theta = synthetic_factor(30_000, f, 97 + f, 0.2)
+    check_lockstep(c, orc, rowptr, colidx, vals, len(lengths), 30_000, f, 0.05, theta,
+                   f"parts of 32 ({form}) edge lengths f={f}")
+    c.close()
+
+
+@pytest.mark.parametrize("f", [16, 100])
+def test_accumulation_through_memory(orc, f):
+    """The ablation form of the paper's register accumulation (section 5.2): parts of one
+    pipeline group, 16 ratings, so that A_u is accumulated in the wave's slot in device memory
+    every 16 ratings instead of staying in registers for the whole row.  Same results."""
+    c = _env_ctx(ALS_PART_ENTRIES=16)
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=785)
+    check_lockstep(c, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"memory accumulation f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 786, 1.0 / np.sqrt(f))
+    check_lockstep(c, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"memory accumulation f={f} item")
+    c.close()
+
+
+@pytest.mark.parametrize("f", [4, 16, 32, 100, 128])
+def test_lds_staged_gather_form(orc, f):
+    """The ablation form of the gather that stages theta rows through LDS (ALS_GATHER=lds; f a
+    multiple of 4): lockstep against the oracle on both sides and on edge row lengths."""
+    c = _env_ctx(ALS_GATHER="lds")
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
+                   plant_f=16, seed=787)
+    check_lockstep(c, orc, p.rowptr, p.colidx, p.vals, p.m, p.n, f, 0.05, p.theta0,
+                   f"lds-staged gather f={f} user")
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, f, 788, 1.0 / np.sqrt(f))
+    check_lockstep(c, orc, colptr, rowidx, vt, p.n, p.m, f, 0.05, xin,
+                   f"lds-staged gather f={f} item")
+    lengths = [0, 1, 2, f - 1, f, f + 1, 47, 48, 49, 95, 96, 97, 0, 1000, 4097, 0]
+    rowptr, colidx, vals = _handmade(lengths, 20_000, seed=f + 15)
+    theta = synthetic_factor(20_000, f, 99 + f, 0.2)
+    check_lockstep(c, orc, rowptr, colidx, vals, len(lengths), 20_000, f, 0.05, theta,
+                   f"lds-staged gather edge lengths f={f}")
+    c.close()
+
+
+def test_lds_staged_gather_needs_f_multiple_of_4():
+    from paper_1603_03820_amd import als
+    c = _env_ctx(ALS_GATHER="lds")
+    dev = c.device
+    rp = torch.tensor([0, 1], dtype=torch.int64, device=dev)
+    ci = torch.tensor([0], dtype=torch.int32, device=dev)
+    v = torch.tensor([1.0], dtype=torch.float32, device=dev)
+    th = torch.ones(256, dtype=torch.float32, device=dev)
+    x = torch.zeros(256, dtype=torch.float32, device=dev)
+    with pytest.raises(als.ALSError) as ei:
+        als.als_half_sweep(c, rp, ci, v, 1, 1, 7, 0.1, th, x)
+    assert ei.value.code == -2
+    c.close()
+
+
+def test_parts_leave_short_pieces_bit_identical(ctx):
+    """Pieces no longer than one part run exactly as before: with parts of 65,536 entries (the
+    default) and of 2^20, the movie-small half-sweeps are bit-identical."""
+    c = _env_ctx(ALS_PART_ENTRIES=1 << 20)
+    p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=100, model="movie",
+                   plant_f=16, seed=783)
+    colptr, rowidx, vt = p.csc()
+    xin = synthetic_factor(p.m, 100, 784, 0.1)
+    a = gpu_half_sweep(ctx, colptr, rowidx, vt, p.n, p.m, 100, 0.05, xin)
+    b = gpu_half_sweep(c, colptr, rowidx, vt, p.n, p.m, 100, 0.05, xin)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    c.close()
+
+
 @pytest.mark.parametrize("f", [16, 100])
 def test_long_row_in_small_chunks(ctx, orc, f):
     """A very long row at the end of the cost axis is cut by many small chunks; its pieces are
