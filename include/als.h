@@ -122,6 +122,26 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
    room for one RMSE wave per SIMD.  ALS_ERR_INVALID_ARG outside 0..8. */
 int als_rmse_waves(als_ctx* ctx, int32_t waves_per_simd);
 
+/*
+ * For callers that cannot allocate device memory or hold a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the training RMSE of
+ * als_rmse, the same kernels, chunks and summation order (so the same value as als_rmse at its
+ * default width), on `device` without a context.  Its scratch -- the chunk counter and one fp64
+ * partial per chunk, 256 + 8 x 32 x (compute units) bytes -- is a fixed array of the library
+ * of 82,176 bytes (devices of up to 320 compute units; a larger device gets ALS_ERR_WORKSPACE),
+ * one copy per device, held until the process ends.  The call allocates nothing: no hipMalloc,
+ * no hipFree, no allocating library routine.  Set-up (the device query and the array's device
+ * address) runs once per device, in als_init on that device or else in the first call; later
+ * calls only check arguments and queue three kernels on `stream` (the counter is cleared by a
+ * kernel, not a memset).  Every call on one device shares that device's array: calls that
+ * overlap in time on one device -- on different streams or from different host threads --
+ * race and give undefined results; the caller orders them.  Arguments, layout and errors as
+ * als_rmse; ALS_ERR_DEVICE if `device` is invalid or not a gfx950 device.
+ */
+int als_rmse_noalloc(int device, const int64_t* rowptr, const int32_t* colidx,
+                     const float* vals, int64_t m, int64_t n, int32_t f, const float* x,
+                     const float* theta, double* rmse_out, void* stream);
+
 /* Synchronise `stream`, then return (and reset to 0) the number of rows found not positive
    definite by half-sweeps since the previous call. */
 int als_status(als_ctx* ctx, void* stream, int64_t* nonspd_rows);

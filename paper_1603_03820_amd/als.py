@@ -19,7 +19,8 @@ ALS_OK = 0
 ALS_F_MAX = 128
 EXPORTED = ("als_workspace_bytes", "als_init", "als_destroy", "als_half_sweep", "als_rmse",
             "als_status", "als_plan", "als_csr_to_csc", "als_rmse_waves", "als_gather_dump",
-            "als_profile_begin", "als_profile_end", "als_last_hip_error", "als_strerror")
+            "als_profile_begin", "als_profile_end", "als_last_hip_error", "als_strerror",
+            "als_rmse_noalloc")
 
 
 class ALSError(RuntimeError):
@@ -43,6 +44,7 @@ def _load():
     lib.als_destroy.argtypes = [P]
     lib.als_half_sweep.argtypes = [P, P, P, P, i64, i64, i32, f32, P, P, P]
     lib.als_rmse.argtypes = [P, P, P, P, i64, i64, i32, P, P, P, P]
+    lib.als_rmse_noalloc.argtypes = [ctypes.c_int, P, P, P, i64, i64, i32, P, P, P, P]
     lib.als_status.argtypes = [P, P, ctypes.POINTER(i64)]
     lib.als_plan.argtypes = [P, P, i64, i32, P, i64, P, P]
     lib.als_csr_to_csc.argtypes = [P, P, P, P, i64, i64, P, P, P, P]
@@ -55,7 +57,7 @@ def _load():
     lib.als_strerror.restype = ctypes.c_char_p
     for fn in ("als_init", "als_destroy", "als_half_sweep", "als_rmse", "als_status", "als_plan",
                "als_csr_to_csc", "als_rmse_waves", "als_gather_dump", "als_profile_begin",
-               "als_profile_end", "als_last_hip_error"):
+               "als_profile_end", "als_last_hip_error", "als_rmse_noalloc"):
         getattr(lib, fn).restype = ctypes.c_int
     return lib
 
@@ -153,6 +155,21 @@ def als_rmse(ctx: Context, rowptr, colidx, vals, m: int, n: int, f: int, x, thet
                        _dev(theta, torch.float32, "theta", n * f),
                        _dev(out, torch.float64, "out", 1), _stream(ctx.device, stream))
     _check("als_rmse", rc, ctx.handle)
+    return out
+
+
+def als_rmse_noalloc(device: int, rowptr, colidx, vals, m: int, n: int, f: int, x, theta, out,
+                     stream=None):
+    """als_rmse without a context or workspace: the library's fixed per-device scratch, no
+    allocation in the call.  `out` (a 1-element float64 device tensor) is the caller's."""
+    dev = torch.device("cuda", device)
+    rc = _lib.als_rmse_noalloc(device, _dev(rowptr, torch.int64, "rowptr", m + 1),
+                               _dev(colidx, torch.int32, "colidx"),
+                               _dev(vals, torch.float32, "vals"), m, n, f,
+                               _dev(x, torch.float32, "x", m * f),
+                               _dev(theta, torch.float32, "theta", n * f),
+                               _dev(out, torch.float64, "out", 1), _stream(dev, stream))
+    _check("als_rmse_noalloc", rc)
     return out
 
 

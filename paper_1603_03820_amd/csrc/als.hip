@@ -36,6 +36,7 @@
 #include <cstdlib>
 #include <climits>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "als.h"
@@ -2033,6 +2034,57 @@ void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, con
     }
 }
 
+// ---------------------------------------------------------- fixed scratch (no workspace) ---
+
+// als_rmse_noalloc's scratch: the claim counter (at 0) and one fp64 partial per RMSE chunk (at
+// 256), for devices of up to kNoAllocMaxCUs compute units.  Each device holds its own copy of
+// the array; host code reaches a device's copy only through the address hipGetSymbolAddress
+// returns with that device current (the array's name is a host-side stand-in).
+constexpr int kNoAllocMaxCUs = 320;
+constexpr size_t kNoAllocPartials = 256;
+constexpr size_t kNoAllocScratchBytes =
+    kNoAllocPartials + sizeof(double) * (size_t)kNoAllocMaxCUs * kRmseWavesPerCU;
+constexpr int kNoAllocMaxDevices = 64;
+
+struct NoAllocDevice {
+    std::once_flag once;
+    int rc = ALS_ERR_DEVICE;
+    unsigned char* ptr = nullptr;   // this device's copy of the scratch array
+    int cus = 0;
+};
+NoAllocDevice g_noalloc[kNoAllocMaxDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+// Once per device, with that device current: its compute units and the device address of its
+// copy of `scratch`.  Called by als_init and by the first als_rmse_noalloc on a device.
+int noalloc_setup(int device) {
+    if (device < 0 || device >= kNoAllocMaxDevices) return ALS_ERR_DEVICE;
+    NoAllocDevice& d = g_noalloc[device];
+    std::call_once(d.once, [&d, device]() {
+        int n = 0;
+        if (hipGetDeviceCount(&n) != hipSuccess || device >= n) return;
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, device) != hipSuccess) return;
+        if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return;
+        DeviceGuard guard(device);
+        if (!guard.ok) return;
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            d.rc = ALS_ERR_HIP;
+            return;
+        }
+        d.ptr = (unsigned char*)ptr;
+        d.cus = prop.multiProcessorCount;
+        d.rc = ALS_OK;
+    });
+    return d.rc;
+}
+
 int rmse_check(const int64_t* rowptr, const int32_t* colidx, const float* vals, int64_t m,
                int64_t n, int32_t f, const float* x, const float* theta, const double* rmse_out) {
     if (f < 1 || f > ALS_F_MAX) return ALS_ERR_UNSUPPORTED_F;
@@ -2124,6 +2176,7 @@ int als_init(als_ctx** out, int device, void* workspace, size_t workspace_bytes,
         ctx->part_groups = groups;
     }
     ctx->nb_max = nb_of(f_max);
+    if (int su = noalloc_setup(device); su != ALS_OK) { delete ctx; return su; }
     if (ctx->staged_gather) {   // the staged form's residency bounds the partition's W
         DeviceGuard g2(device);
         for (int nb = 1; nb <= ctx->nb_max; ++nb) {
@@ -2253,6 +2306,25 @@ int als_rmse(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, const f
                                (double*)(ctx->ws + ctx->lay.rmse),
                                (unsigned*)(ctx->ws + ctx->lay.status + 128), rmse_out);
     return e == hipSuccess ? ALS_OK : fail_hip(ctx, e);
+}
+
+int als_rmse_noalloc(int device, const int64_t* rowptr, const int32_t* colidx,
+                     const float* vals, int64_t m, int64_t n, int32_t f, const float* x,
+                     const float* theta, double* rmse_out, void* stream) {
+    const int rc = rmse_check(rowptr, colidx, vals, m, n, f, x, theta, rmse_out);
+    if (rc != ALS_OK) return rc;
+    const int su = noalloc_setup(device);
+    if (su != ALS_OK) return su;
+    const NoAllocDevice& d = g_noalloc[device];
+    // the partials of the device's fixed chunk count must fit the fixed array
+    if (kNoAllocPartials + sizeof(double) * (size_t)d.cus * kRmseWavesPerCU > kNoAllocScratchBytes)
+        return ALS_ERR_WORKSPACE;
+    DeviceGuard guard(device);
+    if (!guard.ok) return ALS_ERR_DEVICE;
+    hipError_t e = rmse_launch(d.cus, 0, false, (hipStream_t)stream, rowptr, colidx, vals, m, n,
+                               f, x, theta, (double*)(d.ptr + kNoAllocPartials),
+                               (unsigned*)d.ptr, rmse_out);
+    return e == hipSuccess ? ALS_OK : ALS_ERR_HIP;
 }
 
 int als_status(als_ctx* ctx, void* stream, int64_t* nonspd_rows) {
