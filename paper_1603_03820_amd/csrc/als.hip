@@ -288,12 +288,20 @@ __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc
 // Gather forms (the second template argument).
 constexpr int kFormGlobal = 0, kFormBuffer = 1, kFormStaged = 2;
 
+// One entry of the index ring: the entry's gather word (a byte offset or a row address, as the
+// gather form defines it) and its rating.
+template <class W>
+struct RingEntryT {
+    W e;
+    float r;
+};
+
 template <int NB, int BUF, int P = 0>
 struct Gather;
 
 template <int NB, int P>
 struct Gather<NB, kFormBuffer, P> {
-    static constexpr bool kMasked = false;
+    using Entry = RingEntryT<int>;
     static constexpr int kBuf = NB + (P > 1 ? P - 1 : 0);   // operand values per step
     __amdgpu_buffer_rsrc_t rs;
     unsigned fbytes, size, lo, llast;
@@ -345,35 +353,60 @@ struct Gather<NB, kFormBuffer, P> {
     }
 };
 
-template <int NB>
-struct Gather<NB, kFormGlobal, 0> {
-    static constexpr bool kMasked = true;
-    static constexpr int kBuf = NB;
-    const float* theta;
-    int f;
-    int jl[NB];
-    bool jv[NB], jr[NB];
-    __device__ __forceinline__ Gather(const float* th, int64_t, int f_, int c, float* = nullptr)
-        : theta(th), f(f_) {
+// A row of zeros, read in place of theta_v by the 64-bit gather for entries past a piece's end.
+__device__ float g_zero_row[16 * kMaxNB];
+
+// Gather<NB, kFormGlobal, P>, for any size of theta: 64-bit global loads.  The gather word of an
+// entry is its row's address (g_zero_row past the piece's end, so such entries gather zeros);
+// lane (g, c) reads block I < NB-1 at that address + 4 (16 I + c), with 64 I as the
+// instruction's immediate offset.  In the last block a padding lane reads column 0 and the value
+// is replaced (by the rating in column f, else by 0); the quad operands read their columns
+// 16 (NB-1) + 4 p + (c & 3) as in the buffer form.
+template <int NB, int P>
+struct Gather<NB, kFormGlobal, P> {
+    using Entry = RingEntryT<uint64_t>;
+    static constexpr int kBuf = NB + (P > 1 ? P - 1 : 0);
+    typedef const __attribute__((address_space(1))) float* gptr;
+    uint64_t base, zero;
+    unsigned fbytes, lo, llast;
+    bool jpad, jr, jq;
+    unsigned lw[P > 1 ? P - 1 : 1];
+    __device__ __forceinline__ Gather(const float* theta, int64_t, int f, int c,
+                                      float* = nullptr) {
+        base = (uint64_t)theta;
+        zero = (uint64_t)g_zero_row;
+        fbytes = 4u * (unsigned)f;
+        lo = 4u * (unsigned)c;
+        const int jlast = 16 * (NB - 1) + c;
+        jpad = jlast >= f;
+        llast = jpad ? 0u : 4u * (unsigned)jlast;
+        jr = jlast == f;
+        jq = (c & 3) == 0;
 #pragma unroll
-        for (int I = 0; I < NB; ++I) {
-            const int j = 16 * I + c;
-            jv[I] = (I < NB - 1) || j < f;
-            jr[I] = (I == NB - 1) && j == f;
-            jl[I] = jv[I] ? j : 0;
+        for (int p = 0; p < (P > 1 ? P - 1 : 1); ++p)
+            lw[p] = 4u * (unsigned)(16 * (NB - 1) + 4 * p + (c & 3));
+    }
+    __device__ __forceinline__ uint64_t word(int col, bool valid) const {
+        return valid ? base + (uint64_t)(unsigned)col * fbytes : zero;
+    }
+    __device__ __forceinline__ void issue(uint64_t e, float (&v)[kBuf]) const {
+        const gptr pl = (gptr)(e + lo);
+#pragma unroll
+        for (int I = 0; I < NB - 1; ++I) v[I] = pl[16 * I];
+        v[NB - 1] = *(gptr)(e + llast);
+#pragma unroll
+        for (int p = 0; p + 1 < P; ++p) v[NB + p] = *(gptr)(e + lw[p]);
+    }
+    __device__ __forceinline__ void operands(const float (&B)[kBuf], float r, bool,
+                                             float (&v)[NB], float (&w)[P > 0 ? P : 1]) const {
+#pragma unroll
+        for (int I = 0; I < NB - 1; ++I) v[I] = B[I];
+        v[NB - 1] = jpad ? (jr ? r : 0.f) : B[NB - 1];
+        if constexpr (P > 0) {
+#pragma unroll
+            for (int p = 0; p + 1 < P; ++p) w[p] = B[NB + p];
+            w[P - 1] = jq ? r : 0.f;
         }
-    }
-    __device__ __forceinline__ int word(int col, bool valid) const { return valid ? col : 0; }
-    __device__ __forceinline__ void issue(int e, float (&v)[NB]) const {
-        const float* tp = theta + (size_t)(unsigned)e * (size_t)f;
-#pragma unroll
-        for (int I = 0; I < NB; ++I) v[I] = tp[jl[I]];
-    }
-    __device__ __forceinline__ void operands(const float (&B)[NB], float r, bool ok,
-                                             float (&v)[NB], float (&)[1]) const {
-        const float rr = ok ? r : 0.f;
-#pragma unroll
-        for (int I = 0; I < NB; ++I) v[I] = (ok && jv[I]) ? B[I] : (jr[I] ? rr : 0.f);
     }
 };
 
@@ -388,7 +421,7 @@ constexpr int stage_floats(int nb) { return 4 * 16 * nb; }
 
 template <int NB>
 struct Gather<NB, kFormStaged, 0> {
-    static constexpr bool kMasked = false;
+    using Entry = RingEntryT<int>;
     static constexpr int kBuf = 8;
     __amdgpu_buffer_rsrc_t rs;
     unsigned fbytes, size, o0, o1;
@@ -436,18 +469,14 @@ struct Gather<NB, kFormStaged, 0> {
     }
 };
 
-// One ring entry: gather word and rating.
-struct RingEntry {
-    int e;
-    float r;
-};
-
 // Entry `first + lane` of the piece starting at kbeg (lanes below kBatch; past the end: the
 // invalid gather word and rating 0).
 template <class G>
-__device__ __forceinline__ RingEntry load_entry(const G& gat, const int32_t* __restrict__ colidx,
-                                                const float* __restrict__ vals, int64_t kbeg,
-                                                int64_t total, int64_t first, int lane) {
+__device__ __forceinline__ typename G::Entry load_entry(const G& gat,
+                                                        const int32_t* __restrict__ colidx,
+                                                        const float* __restrict__ vals,
+                                                        int64_t kbeg, int64_t total,
+                                                        int64_t first, int lane) {
     const bool valid = lane < kBatch && first + lane < total;
     int col = 0;
     float rv = 0.f;
@@ -455,12 +484,13 @@ __device__ __forceinline__ RingEntry load_entry(const G& gat, const int32_t* __r
         col = colidx[kbeg + first + lane];
         rv = vals[kbeg + first + lane];
     }
-    return RingEntry{gat.word(col, valid), rv};
+    return typename G::Entry{gat.word(col, valid), rv};
 }
 
 // The first two index batches of a row piece, loaded ahead of time into registers.
+template <class G>
 struct RowIndex {
-    RingEntry q0, q1;
+    typename G::Entry q0, q1;
 };
 
 // The gather pipeline's in-flight state: operand values and ratings of the steps in flight
@@ -474,7 +504,7 @@ struct Inflight {
 template <class G>
 __device__ __forceinline__ void gram_prefetch(const G& gat, const int32_t* __restrict__ colidx,
                                               const float* __restrict__ vals, int64_t kbeg,
-                                              int64_t kend, int lane, RowIndex& ix) {
+                                              int64_t kend, int lane, RowIndex<G>& ix) {
     ix.q0 = load_entry(gat, colidx, vals, kbeg, kend - kbeg, 0, lane);
     ix.q1 = load_entry(gat, colidx, vals, kbeg, kend - kbeg, kBatch, lane);
 }
@@ -482,8 +512,9 @@ __device__ __forceinline__ void gram_prefetch(const G& gat, const int32_t* __res
 // Put a piece's first two batches into ring slots 0 and 1 (the ring must be idle) and issue
 // the gathers of its first kDepth steps.
 template <class G>
-__device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, RingEntry* ring,
-                                           int lane, Inflight<G::kBuf>& in) {
+__device__ __forceinline__ void gram_stage(const G& gat, const RowIndex<G>& ix,
+                                           typename G::Entry* ring, int lane,
+                                           Inflight<G::kBuf>& in) {
     const int g = lane >> 4;
     if (lane < kBatch) {
         ring[lane] = ix.q0;
@@ -492,7 +523,7 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kDepth; ++j) {
-        const RingEntry q = ring[4 * j + g];
+        const typename G::Entry q = ring[4 * j + g];
         in.r[j] = q.r;
         gat.issue(q.e, in.b[j]);
     }
@@ -502,8 +533,8 @@ __device__ __forceinline__ void gram_stage(const G& gat, const RowIndex& ix, Rin
 // adds nothing) after issuing step s0 + J + kDepth into buffer (J + kDepth) mod kGroup (free: its
 // step ran at sub-step J - 1).
 template <int J, class G, class Body>
-__device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* ring, int rq, int s0,
-                                              int total, int g, Inflight<G::kBuf>& in,
+__device__ __forceinline__ void pipe_substeps(const G& gat, const typename G::Entry* ring, int rq,
+                                              int s0, int total, int g, Inflight<G::kBuf>& in,
                                               Body& body) {
     if constexpr (J < kGroup) {
         constexpr int JN = (J + kDepth) % kGroup;
@@ -511,7 +542,7 @@ __device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* rin
         __builtin_amdgcn_sched_barrier(0);
         int pos = rq + 4 * J;
         if (pos >= kRing) pos -= kRing;
-        const RingEntry e = ring[pos + g];
+        const typename G::Entry e = ring[pos + g];
         in.r[JN] = e.r;
         gat.issue(e.e, in.b[JN]);
         body.template run<J>();
@@ -530,14 +561,14 @@ __device__ __forceinline__ void pipe_substeps(const G& gat, const RingEntry* rin
 template <class G, class Body>
 __device__ __forceinline__ void pipe_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
-                                          int64_t kend, RingEntry* ring, int lane,
+                                          int64_t kend, typename G::Entry* ring, int lane,
                                           Inflight<G::kBuf>& in, Body& body) {
     const int g = lane >> 4;
     // a row has fewer than 2^31 entries (its columns are distinct int32 indices)
     const int total = (int)(kend - kbeg);
     const int nsteps = (total + 3) >> 2;
     const int ngroups = (nsteps + kGroup - 1) / kGroup;
-    RingEntry nq{0, 0.f};
+    typename G::Entry nq{};
     int qb = 0, k = 0;       // group's position in its batch; batch of the group's steps
     int rq = 4 * kDepth;     // ring position of the first step issued in the group
     for (int q = 0; q < ngroups; ++q) {
@@ -683,7 +714,7 @@ template <int NB, int P, bool PARTS, class G>
 __device__ __forceinline__ void gram_loop(const G& gat, const int32_t* __restrict__ colidx,
                                           const float* __restrict__ vals, int64_t kbeg,
                                           int64_t kend, f4 (&acc)[ntiles(NB)],
-                                          QuadAcc<NB, P>& qa, RingEntry* ring, int lane,
+                                          QuadAcc<NB, P>& qa, typename G::Entry* ring, int lane,
                                           Inflight<G::kBuf>& in, void* quad_scratch,
                                           float* wslot, int part_mask) {
     GramBody<NB, P, G, PARTS> body{part_mask, gat, acc, qa, quad_scratch, wslot, lane, {}, {},
@@ -736,7 +767,7 @@ __global__ __launch_bounds__(kWave) void k_gather_dump(
     const float* __restrict__ vals, const float* __restrict__ theta, int64_t n, int f, int64_t u,
     float* __restrict__ out, int64_t limit) {
     using G = Gather<NB, BUF, P>;
-    __shared__ RingEntry ring[kRing];
+    __shared__ typename G::Entry ring[kRing];
     __shared__ __attribute__((aligned(16))) float stage[BUF == kFormStaged ? stage_floats(NB) : 4];
     const int lane = threadIdx.x;
     if constexpr (BUF == kFormStaged) {
@@ -745,7 +776,7 @@ __global__ __launch_bounds__(kWave) void k_gather_dump(
     }
     const G gat(theta, n, f, lane & 15, stage);
     const int64_t kbeg = rowptr[u], kend = rowptr[u + 1];
-    RowIndex ix;
+    RowIndex<G> ix;
     Inflight<G::kBuf> in;
     gram_prefetch(gat, colidx, vals, kbeg, kend, lane, ix);
     gram_stage(gat, ix, ring, lane, in);
@@ -1101,8 +1132,9 @@ void k_herm_solve(
         if (longest > n) longest = n;
         if ((longest > (int64_t)kEntriesPerGroup * (part_mask + 1)) != PARTS) return;
     }
+    using G = Gather<NB, BUF, P>;
     __shared__ __attribute__((aligned(16))) SolveLds<NB> lds;
-    __shared__ RingEntry ring[kRing];
+    __shared__ typename G::Entry ring[kRing];
     __shared__ __attribute__((aligned(16))) float stage[BUF == kFormStaged ? stage_floats(NB) : 4];
     const int lane = threadIdx.x;
     if constexpr (BUF == kFormStaged) {
@@ -1144,8 +1176,8 @@ void k_herm_solve(
         };
         Piece cur;
         if (!next_piece(u0, cur)) continue;
-        RowIndex ix;
-        Inflight<Gather<NB, BUF, P>::kBuf> in;
+        RowIndex<G> ix;
+        Inflight<G::kBuf> in;
         gram_prefetch(gat, colidx, vals, cur.beg, cur.end, lane, ix);
         gram_stage(gat, ix, ring, lane, in);
         for (;;) {
@@ -1374,7 +1406,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
     const float* __restrict__ theta, int C, double* __restrict__ partial,
     unsigned* __restrict__ claim) {
     using G = Gather<NB, BUF, 0>;
-    __shared__ RingEntry ring[kRing];
+    __shared__ typename G::Entry ring[kRing];
     const int lane = threadIdx.x, c = lane & 15;
     const int64_t nnz = rowptr[m];
     // No lane-0-only region in this loop: every lane takes part in the claim (lane 0 adds one,
@@ -1397,7 +1429,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
             int64_t u = lo;
             int64_t pb = kb, pe = rowptr[u + 1] < ke ? rowptr[u + 1] : ke;
             const G gat(theta, n, f, c);
-            RowIndex ix;
+            RowIndex<G> ix;
             Inflight<G::kBuf> in;
             gram_prefetch(gat, colidx, vals, pb, pe, lane, ix);
             gram_stage(gat, ix, ring, lane, in);
@@ -1741,12 +1773,20 @@ int occupancy_waves(int cus, int* waves) {
                                                                   kQuad2<NB> ? 2 : 1, false>
                                       : nullptr,
                            (const void*)k_herm_solve<NB, kFormGlobal, 0, false>,
+                           (const void*)k_herm_solve<NB, kFormGlobal, 1, false>,
+                           kQuad2<NB> ? (const void*)k_herm_solve<NB, kFormGlobal,
+                                                                  kQuad2<NB> ? 2 : 1, false>
+                                      : nullptr,
                            (const void*)k_herm_solve<NB, kFormBuffer, 0, true>,
                            (const void*)k_herm_solve<NB, kFormBuffer, 1, true>,
                            kQuad2<NB> ? (const void*)k_herm_solve<NB, kFormBuffer,
                                                                   kQuad2<NB> ? 2 : 1, true>
                                       : nullptr,
-                           (const void*)k_herm_solve<NB, kFormGlobal, 0, true>};
+                           (const void*)k_herm_solve<NB, kFormGlobal, 0, true>,
+                           (const void*)k_herm_solve<NB, kFormGlobal, 1, true>,
+                           kQuad2<NB> ? (const void*)k_herm_solve<NB, kFormGlobal,
+                                                                  kQuad2<NB> ? 2 : 1, true>
+                                      : nullptr};
     for (const void* k : forms) {
         if (!k) continue;
         int b = 0;
@@ -1991,7 +2031,13 @@ void launch_sweep(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, co
             launch_herm<NB, kFormBuffer, 0>(W, st, a);
         }
     } else {
-        launch_herm<NB, kFormGlobal, 0>(W, st, a);
+        if (quads == 1) {
+            launch_herm<NB, kFormGlobal, 1>(W, st, a);
+        } else if (quads == 2) {
+            if constexpr (kQuad2<NB>) launch_herm<NB, kFormGlobal, 2>(W, st, a);
+        } else {
+            launch_herm<NB, kFormGlobal, 0>(W, st, a);
+        }
     }
     if (ev) (void)hipEventRecord(ev[2], st);
     if (C > 1) {
@@ -2029,8 +2075,16 @@ void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, con
             hipLaunchKernelGGL((k_gather_dump<NB, true, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, n, f, u, out, limit);
     } else {
-        hipLaunchKernelGGL((k_gather_dump<NB, false, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
-                           colidx, vals, theta, n, f, u, out, limit);
+        if (quads == 1)
+            hipLaunchKernelGGL((k_gather_dump<NB, kFormGlobal, 1>), dim3(1), dim3(kWave), 0, st,
+                               rowptr, colidx, vals, theta, n, f, u, out, limit);
+        else if (quads == 2) {
+            if constexpr (kQuad2<NB>)
+                hipLaunchKernelGGL((k_gather_dump<NB, kFormGlobal, 2>), dim3(1), dim3(kWave), 0,
+                                   st, rowptr, colidx, vals, theta, n, f, u, out, limit);
+        } else
+            hipLaunchKernelGGL((k_gather_dump<NB, kFormGlobal, 0>), dim3(1), dim3(kWave), 0, st,
+                               rowptr, colidx, vals, theta, n, f, u, out, limit);
     }
 }
 

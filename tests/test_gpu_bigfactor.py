@@ -6,7 +6,8 @@ Hugewiki-shaped workload gathers from a 20 GB X).  Here the factor is 3.1-3.2 GB
 matrix holds only ~10^5 ratings, so the oracle checks every row in seconds: most columns lie
 past the first 2 GiB of the factor, and a few rows rate only the factor's last columns.
 Checked: the half-sweep per row (<= 1e-3 against the fp64 oracle), the training RMSE (1e-6
-relative) and the gather stage bit for bit (als_gather_dump) on rows at the factor's end.
+relative) and the gather stage bit for bit (als_gather_dump) on rows at the factor's end, the
+quad-form operands included.
 """
 import numpy as np
 import pytest
@@ -15,6 +16,7 @@ import torch
 import oracle
 import synth
 from tests.gpu_util import log, row_rel_err, to_dev
+from tests.test_gpu_gather import expected, quads
 
 pytestmark = pytest.mark.gpu
 
@@ -89,14 +91,6 @@ def test_factor_above_2gib(ctx, f, n):
         got = als.als_gather_dump(ctx, rp, ci, v, m, n, f, th, u, k1 - k0)
         torch.cuda.synchronize()
         got = got.cpu().numpy()
-        nb = f // 16 + 1
-        cols = colidx[k0:k1]
-        lane = np.arange(16)
-        for I in range(nb):
-            j = 16 * I + lane
-            ref = np.zeros((k1 - k0, 16), np.float32)
-            ref[:, j < f] = theta[cols][:, j[j < f]]
-            ref[:, j == f] = vals[k0:k1][:, None]
-            assert np.array_equal(got[:, I].view(np.uint32), ref.view(np.uint32)), (u, I)
-        assert np.array_equal(got[:, nb + 2].view(np.uint32),
-                              np.repeat(vals[k0:k1][:, None], 16, 1).view(np.uint32)), u
+        ref = expected(theta, colidx[k0:k1], vals[k0:k1], f, quads(f, "global"))
+        bad = np.argwhere(got.view(np.uint32) != ref.view(np.uint32))
+        assert bad.size == 0, f"row {u}: first mismatches {bad[:5].tolist()}"

@@ -33,7 +33,7 @@ def quads(f, form):
     """Quad operands the library uses for this f and form (0: 16x16 tiles for the last block)."""
     nb = f // 16 + 1
     f_last = f - 16 * (nb - 1)
-    if form in ("global", "tiles", "lds") or f_last not in (0, 4):
+    if form in ("tiles", "lds") or f_last not in (0, 4):
         return 0
     return f_last // 4 + 1
 
@@ -61,6 +61,7 @@ def expected(theta, cols, ratings, f, P):
 @pytest.mark.parametrize("f,form", [(1, "buffer"), (7, "buffer"), (16, "buffer"), (33, "buffer"),
                                     (100, "buffer"), (100, "tiles"), (100, "global"),
                                     (112, "buffer"), (128, "buffer"), (128, "global"),
+                                    (7, "global"), (16, "global"), (116, "global"),
                                     (4, "lds"), (32, "lds"), (100, "lds"), (128, "lds")])
 def test_gather_dump_bit_exact(f, form):
     from paper_1603_03820_amd import als
