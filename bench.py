@@ -402,7 +402,8 @@ def ablation_bench(args):
     variants = [
         ("buffer", "quad", "registers", {}),
         ("buffer", "tiles", "registers", {"ALS_LAST_BLOCK": "tiles"}),
-        ("global", "tiles", "registers", {"ALS_GATHER": "global"}),
+        ("global", "quad", "registers", {"ALS_GATHER": "global"}),
+        ("global", "tiles", "registers", {"ALS_GATHER": "global", "ALS_LAST_BLOCK": "tiles"}),
         ("lds-staged", "tiles", "registers", {"ALS_GATHER": "lds"}),
         ("buffer", "quad", "memory every 16 ratings", {"ALS_PART_ENTRIES": "16"}),
     ]
