@@ -178,3 +178,34 @@ def test_bench_traffic_is_tied_to_workload_and_source():
     assert bench.measured_traffic(workload.replace("f=100", "f=32")) is None
     assert bench.measured_traffic(workload.replace("movie", "music")) is None
     assert bench.measured_traffic(workload, tag="music_f100") is None
+
+
+def test_bench_roofline_bound_rule():
+    """The bench's bound: min(FP32 peak, HBM peak x AI): HBM below the ridge (19.7 flop/B),
+    the FP32 datapath above it; and the committed counter bytes are found per workload and side
+    while the kernel source is the one they were taken on."""
+    import hashlib
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_mod2", os.path.join(ROOT, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    ridge = bench.FP32_PEAK_TFLOPS * 1e3 / bench.HBM_PEAK_GBS
+    assert abs(ridge - 19.66) < 0.01
+    b, peak, ai = bench.roofline_bound(9.0e12, 1e12)          # AI 9: HBM
+    assert b == "hbm" and abs(peak - 72.0) < 1e-9 and ai == 9.0
+    b, peak, _ = bench.roofline_bound(30.0e12, 1e12)          # AI 30: FP32
+    assert b == "mfma" and peak == bench.FP32_PEAK_TFLOPS
+    # compulsory bytes of a half-sweep: indices + ratings, row pointers, both factors once
+    assert bench.algorithmic_bytes(10, 3, 5, 2) == 8 * 10 + 8 * 4 + 4 * 5 * 2 + 4 * 3 * 2
+    src = hashlib.sha256(open(bench.KERNEL_SRC, "rb").read()).hexdigest()
+    for tag in ("movie_f32", "movie_f64", "movie_f128", "music_f100", "wiki_f100"):
+        path = bench.traffic_file(tag)
+        if not os.path.exists(path):
+            continue
+        kv = dict(l.split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        same = kv["source_sha256"] == src
+        for side in ("user", "item"):
+            got = bench.measured_traffic(kv["workload"], tag, f"bytes_{side}_launch")
+            assert got == (float(kv[f"bytes_{side}_launch"]) if same else None)
+        assert bench.measured_traffic(kv["workload"] + " ", tag) is None

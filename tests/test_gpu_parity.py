@@ -135,7 +135,7 @@ def test_tile_form_of_last_block(ctx_tiles, orc, f):
                    f"tile-form last block movie-small f={f} item")
 
 
-@pytest.mark.parametrize("f", [7, 100, 128])
+@pytest.mark.parametrize("f", [4, 7, 16, 100, 116, 128])
 def test_global_gather_form(ctx_global, orc, f):
     p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
                    plant_f=16, seed=777)
