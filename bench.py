@@ -78,6 +78,8 @@ def parse():
                     help="timed steps per other workload (rank sweep, music, wiki)")
     ap.add_argument("--no-others", action="store_true",
                     help="time the headline workload only (no rank sweep, music or wiki block)")
+    ap.add_argument("--others", default="movie_f32,movie_f64,movie_f128,music,wiki",
+                    help="comma list of the other workloads to time after the headline")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
                          "calibration), then one user and one item half-sweep; no JSON")
@@ -532,7 +534,10 @@ def other_workloads(args, dev, movie):
     from paper_1603_03820_amd import als, driver
     out = {}
     p, dp100 = movie
+    wanted = set(args.others.split(","))
     for f in synth.RANK_SWEEP_F:
+        if f"movie_f{f}" not in wanted:
+            continue
         t0 = time.perf_counter()
         dp = driver.DeviceProblem(p.m, p.n, f, p.lam, dp100.rowptr, dp100.colidx, dp100.vals,
                                   dp100.colptr, dp100.rowidx, dp100.vals_t)
@@ -547,6 +552,8 @@ def other_workloads(args, dev, movie):
               flush=True)
         ctx.close()
     for name in ("music", "wiki"):
+        if name not in wanted:
+            continue
         t0 = time.perf_counter()
         q = synth.config(name)
         ctx = als.Context(0, max(q.f, 16))

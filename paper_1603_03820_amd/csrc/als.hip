@@ -359,9 +359,10 @@ __device__ float g_zero_row[16 * kMaxNB];
 // Gather<NB, kFormGlobal, P>, for any size of theta: 64-bit global loads.  The gather word of an
 // entry is its row's address (g_zero_row past the piece's end, so such entries gather zeros);
 // lane (g, c) reads block I < NB-1 at that address + 4 (16 I + c), with 64 I as the
-// instruction's immediate offset.  In the last block a padding lane reads column 0 and the value
-// is replaced (by the rating in column f, else by 0); the quad operands read their columns
-// 16 (NB-1) + 4 p + (c & 3) as in the buffer form.
+// instruction's immediate offset.  In the last block a padding lane reads a column of the cache
+// line the block's real lanes read -- its first column, or column f - 1 when it has none -- and
+// the value is replaced (by the rating in column f, else by 0); the quad operands read their
+// columns 16 (NB-1) + 4 p + (c & 3) as in the buffer form.
 template <int NB, int P>
 struct Gather<NB, kFormGlobal, P> {
     using Entry = RingEntryT<uint64_t>;
@@ -379,7 +380,8 @@ struct Gather<NB, kFormGlobal, P> {
         lo = 4u * (unsigned)c;
         const int jlast = 16 * (NB - 1) + c;
         jpad = jlast >= f;
-        llast = jpad ? 0u : 4u * (unsigned)jlast;
+        const int jsame = 16 * (NB - 1) < f ? 16 * (NB - 1) : f - 1;
+        llast = 4u * (unsigned)(jpad ? jsame : jlast);
         jr = jlast == f;
         jq = (c & 3) == 0;
 #pragma unroll

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _bench(config, *extra):
     cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--config", config, "--steps", "3",
-           "--warmup", "1", "--no-cpu", "--no-peaks", *extra]
+           "--warmup", "1", "--no-cpu", "--no-peaks", "--no-others", *extra]
     print("[bench]", " ".join(cmd[2:]), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=240)
     assert r.returncode == 0, r.stderr[-3000:]
@@ -56,3 +56,40 @@ def test_bench_line_contract():
     assert rl["traffic"] is None
     cb = out["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
+
+
+@pytest.mark.gpu
+def test_bench_workloads_block():
+    """The bench line's block of other workloads (here the rank sweep and the music shape; the
+    default run adds the wiki shape): per workload and side, the half-sweep and k_herm_solve
+    times from the library's HIP events, the fraction of the FP32 peak, the roofline bound with
+    its AI and where the bytes came from, and the algorithmic Gram / solve flop split."""
+    cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--config", "movie", "--steps", "2",
+           "--warmup", "1", "--no-cpu", "--no-peaks", "--other-steps", "1",
+           "--others", "movie_f32,movie_f64,movie_f128,music"]
+    print("[bench]", " ".join(cmd[2:]), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-3000:]
+    out = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "workloads_error" not in out, out.get("workloads_error")
+    w = out["workloads"]
+    assert set(w) == {"movie_f32", "movie_f64", "movie_f128", "music"}
+    for name, blk in w.items():
+        f = int(blk["workload"].split(" f=")[1].split()[0])
+        assert blk["half_sweeps_per_s"] > 0 and 0 < blk["herm_pair_frac_fp32_peak"] < 1
+        for side in ("user", "item"):
+            s = blk[side]
+            assert 0 < s["herm_ms"] <= s["half_sweep_ms"]
+            assert abs(s["herm_frac_fp32_peak"] - s["herm_tflops"] / 157.3) < 1e-3
+            rl = s["roofline"]
+            assert rl["bound"] in ("hbm", "mfma")
+            herm_fl = s["flops"]["gram"] + (s["rows"] - s["split_rows"]) * (
+                f ** 3 / 3 + 2.5 * f * f + f / 6)
+            assert abs(rl["ai_flop_per_byte"] - herm_fl / rl["bytes"]) <= 0.006
+            peak = min(157.3, 8.0 * herm_fl / rl["bytes"])
+            assert abs(rl["peak_tflops"] - peak) < 0.006
+            assert (rl["bound"] == "hbm") == (peak < 157.3)
+            assert abs(rl["frac"] - s["herm_tflops"] / rl["peak_tflops"]) < 1e-3
+            assert 0 < s["flops"]["gram_share"] < 1
+        # the user side carries the solves: its Gram share is the smaller one
+        assert blk["user"]["flops"]["gram_share"] < blk["item"]["flops"]["gram_share"]
