@@ -152,32 +152,41 @@ def measure_peaks(dev):
     lib.peaks_mfma.argtypes = [V, V, i32, i32, V]
     lib.peaks_fma.argtypes = [V, V, i32, i32, V]
     lib.peaks_copy.argtypes = [V, V, i64, i32, V]
+    lib.peaks_pair.argtypes = [V, V, i32, i32, i32, i32, V]
     chains = lib.peaks_chains()
+    per_iter = lib.peaks_fma_per_iter()
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
     st = torch.cuda.current_stream()
     sp = V(st.cuda_stream)
     inp = torch.rand(128, device=dev)
 
-    def best(launch, work):
-        launch()
-        rates = []
+    def best_ms(launch):
+        assert launch() == 0
+        times = []
         for _ in range(3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(st)
-            launch()
+            assert launch() == 0
             e1.record(st)
             e1.synchronize()
-            rates.append(work / (e0.elapsed_time(e1) * 1e-3))
-        return max(rates)
+            times.append(e0.elapsed_time(e1))
+        return min(times)
+
+    def best(launch, work):
+        return work / (best_ms(launch) * 1e-3)
 
     blocks, iters = cus * 8, 20000                      # 2 waves per SIMD
     out = torch.empty(blocks * 256, device=dev)
     mfma = best(lambda: lib.peaks_mfma(V(inp.data_ptr()), V(out.data_ptr()), blocks, iters, sp),
                 blocks * iters * chains * 2048.0)
-    fblocks, fiters = cus * 8, 40000                    # 8 waves per SIMD
+    fblocks, fiters = cus * 8, 5000                     # 8 waves per SIMD
     fout = torch.empty(fblocks * 256, device=dev)
     fma = best(lambda: lib.peaks_fma(V(inp.data_ptr()), V(fout.data_ptr()), fblocks, fiters, sp),
-               fblocks * 256.0 * fiters * chains * 2)
+               fblocks * 256.0 * fiters * per_iter * 2)
+    # one MFMA wave and one VALU wave on every SIMD: alone, then together
+    pout = torch.empty(cus * 512, device=dev)
+    pair = [best_ms(lambda: lib.peaks_pair(V(inp.data_ptr()), V(pout.data_ptr()), cus, 20000,
+                                           20000, mode, sp)) for mode in (1, 2, 3)]
     n4 = (1 << 30) // 16                                # 1 GiB each way
     src = torch.ones(n4 * 4, device=dev)
     dst = torch.empty_like(src)
@@ -187,7 +196,13 @@ def measure_peaks(dev):
     return {"mfma_f32_tflops": round(mfma / 1e12, 2), "valu_f32_fma_tflops": round(fma / 1e12, 2),
             "hbm_copy_gbs": round(copy / 1e9, 1),
             "mfma_clock_ghz": round(mfma / (cus * 256.0) / 1e9, 3),
-            "note": "unpacked FP32 FMA (packed FP32 is not used); copy = read + write bytes"}
+            "mfma_valu_same_simd": {"mfma_only_ms": round(pair[0], 3),
+                                    "valu_only_ms": round(pair[1], 3),
+                                    "both_ms": round(pair[2], 3),
+                                    "both_over_sum": round(pair[2] / (pair[0] + pair[1]), 3)},
+            "note": "unpacked FP32 FMA (packed FP32 is not used); copy = read + write bytes; "
+                    "mfma_valu_same_simd: one MFMA-stream wave and one VALU-stream wave per SIMD, "
+                    "both_over_sum near 1 = the two kinds of work do not overlap"}
 
 
 def csc_build(ctx, dp, p, reps=3):

@@ -276,16 +276,17 @@ __device__ __forceinline__ void quad_to_tiles(const QuadAcc<NB, P>& qa, f4 (&acc
 }
 
 // The theta gather of one step, as MFMA operands: lane (g, c) of block I reads
-// theta_{v_g}[16 I + c], and the lane of column f takes the rating.  Two forms:
-//   Gather<NB, true>, for theta below 2 GiB: raw buffer loads against a descriptor that bounds
+// theta_{v_g}[16 I + c], and the lane of column f takes the rating.  Three forms (the second
+// template argument):
+//   kFormBuffer, for theta below 2 GiB: raw buffer loads against a descriptor that bounds
 //     theta.  The gather word of an entry is its byte offset 4 f v; an entry past the piece's end
 //     gets the buffer size, and the lanes of padding columns add the size to their offset, so
 //     those loads return 0 by the hardware's range check and nothing is masked in the loop.
-//   Gather<NB, false>, for any size: 64-bit global loads; the gather word is the column index,
-//     loads are clamped to valid addresses (row 0 past the end, column 0 for padding) and the
-//     values are masked when consumed.
-// Both issue their loads unconditionally, so they stay in flight across earlier matrix ops.
-// Gather forms (the second template argument).
+//   kFormGlobal, for any size: 64-bit global loads; the gather word is the row's address (a row
+//     of zeros past the piece's end), and padding lanes read a column of their block's cache
+//     line whose value is then replaced (see Gather<NB, kFormGlobal, P>).
+//   kFormStaged, a design alternative kept for the ablation: the rows go through LDS.
+// All issue their loads unconditionally, so they stay in flight across earlier matrix ops.
 constexpr int kFormGlobal = 0, kFormBuffer = 1, kFormStaged = 2;
 
 // One entry of the index ring: the entry's gather word (a byte offset or a row address, as the
@@ -992,7 +993,6 @@ struct Block {
     }
 };
 
-// run-time K -> Block<NB, K>
 // run-time K -> Block<NB, K>.  Each case ends in its own empty asm statement so that the
 // optimiser cannot merge the cases into one access with a run-time tile index (which would move
 // the accumulator tiles out of registers).

@@ -73,9 +73,17 @@ def test_peak_microbenchmarks_build_and_export():
     import ctypes
     from paper_1603_03820_amd import build
     lib = ctypes.CDLL(build.PEAKS_LIB)
-    for fn in ("peaks_mfma", "peaks_fma", "peaks_copy", "peaks_chains"):
+    for fn in ("peaks_mfma", "peaks_fma", "peaks_pair", "peaks_copy", "peaks_chains",
+               "peaks_fma_per_iter"):
         assert hasattr(lib, fn), fn
-    assert lib.peaks_chains() == 8
+    assert lib.peaks_chains() == 8 and lib.peaks_fma_per_iter() == 64
+    # argument checks run before any launch, so they are safe without a GPU
+    V, I = ctypes.c_void_p, ctypes.c_int
+    lib.peaks_pair.argtypes = [V, V, I, I, I, I, V]
+    assert lib.peaks_pair(None, None, 1, 1, 1, 3, None) == -1
+    buf = ctypes.create_string_buffer(4)
+    assert lib.peaks_pair(buf, buf, 1, 1, 1, 0, None) == -1
+    assert lib.peaks_pair(buf, buf, 1, 1, 1, 4, None) == -1
     if not os.path.exists("/opt/rocm/llvm/bin/clang-offload-bundler"):
         pytest.skip("ROCm LLVM tools not installed")
     text = _device_disassembly(build.PEAKS_LIB)
