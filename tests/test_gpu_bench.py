@@ -35,9 +35,10 @@ def test_overlapped_step_matches_serial(config):
 def test_bench_line_contract():
     """One JSON line with the contract's fields: the metric, whole-job value and step time,
     the roofline of the dominant kernel (frac = achieved / peak; no traffic figure for a workload
-    the counters were not taken on) and the oracle's CPU baseline."""
+    the counters were not taken on), the oracle's CPU baseline and the peak microbenchmarks
+    measured in the same run."""
     cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--config", "tiny", "--steps", "2",
-           "--warmup", "1", "--no-peaks"]
+           "--warmup", "1"]
     print("[bench]", " ".join(cmd[2:]), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=240)
     assert r.returncode == 0, r.stderr[-3000:]
@@ -56,6 +57,14 @@ def test_bench_line_contract():
     assert rl["traffic"] is None
     cb = out["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
+    pk = out["peaks_measured"]
+    assert 0 < pk["mfma_f32_tflops"] and 0 < pk["valu_f32_fma_tflops"] and 0 < pk["hbm_copy_gbs"]
+    pair = pk["mfma_valu_same_simd"]
+    assert min(pair["mfma_only_ms"], pair["valu_only_ms"]) > 0
+    assert pair["both_ms"] >= max(pair["mfma_only_ms"], pair["valu_only_ms"]) * 0.95
+    assert abs(pair["both_over_sum"] - pair["both_ms"] /
+               (pair["mfma_only_ms"] + pair["valu_only_ms"])) < 2e-3
+    assert abs(rl["frac_of_measured_mfma"] - rl["achieved"] / pk["mfma_f32_tflops"]) < 1e-3
 
 
 @pytest.mark.gpu
