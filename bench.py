@@ -76,6 +76,8 @@ def parse():
                          "step's update-X, with X double-buffered)")
     ap.add_argument("--other-steps", type=int, default=3,
                     help="timed steps per other workload (rank sweep, music, wiki)")
+    ap.add_argument("--no-share", action="store_true",
+                    help="skip the one-GPU-share timing (GPU 0's nnz-balanced 1/8 of each side)")
     ap.add_argument("--no-others", action="store_true",
                     help="time the headline workload only (no rank sweep, music or wiki block)")
     ap.add_argument("--others", default="movie_f32,movie_f64,movie_f128,music,wiki",
@@ -539,6 +541,52 @@ def time_workload(ctx, dp, theta0, steps, warmup, rowptr, colptr, tag, name):
             "user": user, "item": item}
 
 
+SHARE_GPUS = 8   # the node size whose one-GPU share is timed
+
+
+def share_workload(ctx, dp, theta0, steps, rowptr, colptr, name, gpus=SHARE_GPUS):
+    """One GPU's share of a G-GPU run at the workload's real shape (rows are independent, so G
+    GPUs would take nnz-balanced contiguous row ranges with the other factor replicated): GPU 0's
+    rows [0, u1) of the CSR and columns [0, v1) of the CSC, each holding about nnz / G ratings,
+    half-swept `steps` times against the whole other factor, timed like time_workload.  Also
+    reports the whole matrix's half-sweep per GPU (full / G) for comparison; the gap is what the
+    persistent grid loses on 1 / G of the work (the all-gather of the updated factor is not
+    run)."""
+    import torch
+    from paper_1603_03820_amd import als, driver
+    nnz = int(rowptr[-1])
+    u1 = max(1, int(np.searchsorted(rowptr, nnz / gpus, side="left")))
+    v1 = max(1, int(np.searchsorted(colptr, nnz / gpus, side="left")))
+    x = torch.empty((dp.m, dp.f), dtype=torch.float32, device=theta0.device)
+    driver.update_x(ctx, dp, theta0, x)                   # the replicated X of the item share
+    xs = torch.empty((u1, dp.f), dtype=torch.float32, device=theta0.device)
+    ts = torch.empty((v1, dp.f), dtype=torch.float32, device=theta0.device)
+    user = (dp.rowptr[:u1 + 1], dp.colidx, dp.vals, u1, dp.n, theta0, xs)
+    item = (dp.colptr[:v1 + 1], dp.rowidx, dp.vals_t, v1, dp.m, x, ts)
+    for sd in (user, item):
+        als.als_half_sweep(ctx, *sd[:5], dp.f, dp.lam, sd[5], sd[6])
+    torch.cuda.synchronize()
+    als.als_profile_begin(ctx, 2 * steps)
+    for _ in range(steps):
+        for sd in (user, item):
+            als.als_half_sweep(ctx, *sd[:5], dp.f, dp.lam, sd[5], sd[6])
+    torch.cuda.synchronize()
+    prof = np.array(als.als_profile_end(ctx, 2 * steps)).reshape(steps, 2, 3)
+    assert als.als_status(ctx) == 0
+    out = {"gpus": gpus, "rows_of": "GPU 0 of the node: the first rows of the CSR and the first "
+                                    "columns of the CSC, nnz-balanced"}
+    for k, (side, sd, ptr) in enumerate((("user", user, rowptr[:u1 + 1]),
+                                         ("item", item, colptr[:v1 + 1]))):
+        share_nnz = int(ptr[-1])
+        w = f"{name} share 1/{gpus} {side}: m={sd[3]} n={sd[4]} nnz={share_nnz} f={dp.f}"
+        fig = side_figures(ctx, sd[0], ptr, sd[3], sd[4], share_nnz, dp.f, prof[:, k, 0],
+                           prof[:, k, 1], prof[:, k, 2], "share", side, w)
+        fig["share_rows"], fig["share_nnz"] = sd[3], share_nnz
+        out[side] = fig
+    del x, xs, ts
+    return out
+
+
 def other_workloads(args, dev, movie):
     """The other paper-shaped workloads, measured after the headline: the rank sweep on the
     movie-shaped matrix (f = 32, 64, 128, fresh initial factors), the music shape and the
@@ -577,8 +625,15 @@ def other_workloads(args, dev, movie):
         colptr, rowidx, vt = als.als_csr_to_csc(ctx, rp, ci, v, q.m, q.n, nnz=q.nnz)
         dp = driver.DeviceProblem(q.m, q.n, q.f, q.lam, rp, ci, v, colptr, rowidx, vt)
         gen_s = time.perf_counter() - t0
-        r = time_workload(ctx, dp, t(q.theta0), args.other_steps, 1, q.rowptr,
-                          colptr.cpu().numpy(), f"{name}_f{q.f}", q.name)
+        colptr_h = colptr.cpu().numpy()
+        r = time_workload(ctx, dp, t(q.theta0), args.other_steps, 1, q.rowptr, colptr_h,
+                          f"{name}_f{q.f}", q.name)
+        if not args.no_share:
+            r["share"] = share_workload(ctx, dp, t(q.theta0), args.other_steps, q.rowptr,
+                                        colptr_h, q.name)
+            for side in ("user", "item"):
+                r["share"][side]["full_over_gpus_ms"] = round(
+                    r[side]["half_sweep_ms"] / SHARE_GPUS, 4)
         r["wall_s"] = round(time.perf_counter() - t0, 1)
         r["gen_s"] = round(gen_s, 1)
         out[name] = r
@@ -773,6 +828,13 @@ def main():
         "gen_s": round(t_gen, 1),
     }
     out["csc_build"] = csc_build(ctx, dp, p)
+    if not args.no_share:
+        out["share"] = share_workload(ctx, dp, torch.from_numpy(p.theta0).to(dev),
+                                      max(3, min(args.steps, 10)),
+                                      p.rowptr, csc[0], p.name)
+        for k, side in enumerate(("user", "item")):
+            out["share"][side]["full_over_gpus_ms"] = round(
+                float(np.median(sweep_ms[:, k])) / SHARE_GPUS, 4)
     if not args.no_peaks:
         out["peaks_measured"] = measure_peaks(dev)
         roofline["frac_of_measured_mfma"] = round(

@@ -65,6 +65,19 @@ def test_bench_line_contract():
     assert abs(pair["both_over_sum"] - pair["both_ms"] /
                (pair["mfma_only_ms"] + pair["valu_only_ms"])) < 2e-3
     assert abs(rl["frac_of_measured_mfma"] - rl["achieved"] / pk["mfma_f32_tflops"]) < 1e-3
+    _check_share(out["share"], out["config"]["nnz"])
+
+
+def _check_share(sh, nnz):
+    """GPU 0's share of an 8-GPU node: about nnz / 8 ratings per side, timed like the rest."""
+    assert sh["gpus"] == 8
+    for side in ("user", "item"):
+        s = sh[side]
+        assert s["share_rows"] >= 1 and 0 < s["herm_ms"] <= s["half_sweep_ms"]
+        # the first rows (columns) that reach nnz / 8; one row or column overshoots it
+        assert nnz / 8 <= s["share_nnz"] <= nnz / 8 + 0.05 * nnz
+        # (a tiny share is launch-bound: its fraction of the peak can round to 0)
+        assert 0 <= s["herm_frac_fp32_peak"] < 1 and s["full_over_gpus_ms"] > 0
 
 
 @pytest.mark.gpu
@@ -102,3 +115,6 @@ def test_bench_workloads_block():
             assert 0 < s["flops"]["gram_share"] < 1
         # the user side carries the solves: its Gram share is the smaller one
         assert blk["user"]["flops"]["gram_share"] < blk["item"]["flops"]["gram_share"]
+        if name == "music":
+            nnz = int(blk["workload"].split(" nnz=")[1].split()[0])
+            _check_share(blk["share"], nnz)
