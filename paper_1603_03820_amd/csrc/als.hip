@@ -1407,7 +1407,7 @@ __global__ __launch_bounds__(kWave) void k_rmse_rows(
     const float* __restrict__ vals, int64_t m, int64_t n, int f, const float* __restrict__ x,
     const float* __restrict__ theta, int C, double* __restrict__ partial,
     unsigned* __restrict__ claim) {
-    using G = Gather<NB, BUF, 0>;
+    using G = Gather<NB, BUF ? kFormBuffer : kFormGlobal, 0>;
     __shared__ typename G::Entry ring[kRing];
     const int lane = threadIdx.x, c = lane & 15;
     const int64_t nnz = rowptr[m];
@@ -2067,14 +2067,14 @@ void launch_dump(als_ctx* ctx, const int64_t* rowptr, const int32_t* colidx, con
     } else if (!ctx->global_gather &&
                (uint64_t)n * (uint64_t)f * sizeof(float) <= kBufferGatherMax) {
         if (quads == 1)
-            hipLaunchKernelGGL((k_gather_dump<NB, true, 1>), dim3(1), dim3(kWave), 0, st, rowptr,
+            hipLaunchKernelGGL((k_gather_dump<NB, kFormBuffer, 1>), dim3(1), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, n, f, u, out, limit);
         else if (quads == 2) {
             if constexpr (kQuad2<NB>)
-                hipLaunchKernelGGL((k_gather_dump<NB, true, 2>), dim3(1), dim3(kWave), 0, st,
+                hipLaunchKernelGGL((k_gather_dump<NB, kFormBuffer, 2>), dim3(1), dim3(kWave), 0, st,
                                    rowptr, colidx, vals, theta, n, f, u, out, limit);
         } else
-            hipLaunchKernelGGL((k_gather_dump<NB, true, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
+            hipLaunchKernelGGL((k_gather_dump<NB, kFormBuffer, 0>), dim3(1), dim3(kWave), 0, st, rowptr,
                                colidx, vals, theta, n, f, u, out, limit);
     } else {
         if (quads == 1)
