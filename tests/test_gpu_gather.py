@@ -61,7 +61,8 @@ def expected(theta, cols, ratings, f, P):
 @pytest.mark.parametrize("f,form", [(1, "buffer"), (7, "buffer"), (16, "buffer"), (33, "buffer"),
                                     (100, "buffer"), (100, "tiles"), (100, "global"),
                                     (112, "buffer"), (128, "buffer"), (128, "global"),
-                                    (7, "global"), (16, "global"), (116, "global"),
+                                    (7, "global"), (16, "global"), (21, "global"),
+                                    (47, "global"), (90, "global"), (116, "global"),
                                     (4, "lds"), (32, "lds"), (100, "lds"), (128, "lds")])
 def test_gather_dump_bit_exact(f, form):
     from paper_1603_03820_amd import als

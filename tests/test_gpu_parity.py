@@ -57,7 +57,11 @@ def test_tiny_config_lockstep(ctx, orc):
     check_lockstep(ctx, orc, colptr, rowidx, vt, p.n, p.m, p.f, p.lam, xin, "tiny item side")
 
 
-RANKS = [1, 2, 3, 7, 16, 17, 31, 32, 33, 64, 100, 127, 128]
+# every column-block count (NB = 1..9) and every residue of f mod 16 (the last block's real
+# columns: tile form, quad form with no or one theta quad, the light last-block factor)
+RANKS = [1, 2, 3, 5, 7, 16, 17, 20, 22, 31, 32, 33, 40, 57, 64, 74, 91, 100, 108, 109, 126,
+         127, 128]
+assert {f % 16 for f in RANKS} == set(range(16)) and {f // 16 + 1 for f in RANKS} == set(range(1, 10))
 
 
 @pytest.mark.parametrize("f", RANKS)
@@ -135,7 +139,7 @@ def test_tile_form_of_last_block(ctx_tiles, orc, f):
                    f"tile-form last block movie-small f={f} item")
 
 
-@pytest.mark.parametrize("f", [4, 7, 16, 100, 116, 128])
+@pytest.mark.parametrize("f", [4, 7, 16, 21, 47, 90, 100, 116, 128])
 def test_global_gather_form(ctx_global, orc, f):
     p = synth.make(3_000, 400, 90_000, rows="lognormal", zipf=0.9, f=f, model="movie",
                    plant_f=16, seed=777)
