@@ -84,8 +84,8 @@ def parse():
                     help="comma list of the other workloads to time after the headline")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: a 1 GiB device copy (the bytes-per-KiB "
-                         "calibration), then one user and one item half-sweep and one "
-                         "full-width training RMSE; no JSON")
+                         "calibration), then one user and one item half-sweep, one "
+                         "full-width training RMSE and one device CSR->CSC build; no JSON")
     return ap.parse_args()
 
 
@@ -690,6 +690,7 @@ def main():
         driver.update_x(ctx, dp, theta, x)
         driver.update_theta(ctx, dp, x, theta)
         als.als_rmse(ctx, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, f, x, theta, rmse)
+        als.als_csr_to_csc(ctx, dp.rowptr, dp.colidx, dp.vals, p.m, p.n, nnz=p.nnz)
         torch.cuda.synchronize()
         print("pmc pass done", flush=True)
         return
